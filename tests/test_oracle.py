@@ -1,0 +1,435 @@
+"""Pins of the oracle against facts that do not come from the oracle itself.
+
+Each test checks the float64 oracle against a closed form, an invariant, a
+library routine (PyTorch functional ops, SciPy softmax), or brute force on tiny
+inputs.  Together they are meant to catch a dropped term, a wrong sign or
+index, or a transposed operand anywhere in the oracle.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+import torch.nn.functional as F
+
+import oracle
+import synth
+from oracle import model as om
+
+MICRO = synth.MICRO
+
+
+def micro_model(shape=MICRO, seed=0, int8=False):
+    w = synth.all_weights(shape, "f32", seed)
+    return oracle.OracleModel(shape, w, int8=int8), w
+
+
+# ----------------------------------------------------------------------------
+# An independent reference: PyTorch functional ops, complex-number RoPE, SDPA
+# ----------------------------------------------------------------------------
+
+
+def torch_forward(shape, w, ids, allowed):
+    """Full forward of a sequence (positions 0..n-1) under a boolean mask."""
+    t = lambda a: torch.from_numpy(synth.as_f32(np.asarray(a))).double()
+    n = len(ids)
+    H, dh, d = shape.n_heads, shape.head_dim, shape.d_model
+    half = dh // 2
+    pos = torch.arange(n, dtype=torch.float64)
+    inv = shape.rope_base ** (-torch.arange(half, dtype=torch.float64) * 2.0 / dh)
+    rot = torch.polar(torch.ones(n, half, dtype=torch.float64), pos[:, None] * inv)  # e^{i theta}
+
+    def rope_c(u):  # u [n, H, dh]: pair (j, j + half) as the complex number u_j + i u_{j+half}
+        z = torch.complex(u[..., :half], u[..., half:]) * rot[:, None, :]
+        return torch.cat([z.real, z.imag], dim=-1)
+
+    x = t(w["embed"])[torch.as_tensor(np.asarray(ids, np.int64))]
+    mask = torch.as_tensor(allowed)
+    for lw in w["layers"]:
+        h = F.rms_norm(x, (d,), weight=t(lw["attn_norm"]), eps=shape.eps)
+        q = rope_c(F.linear(h, t(lw["wq"])).view(n, H, dh))
+        k = rope_c(F.linear(h, t(lw["wk"])).view(n, H, dh))
+        v = F.linear(h, t(lw["wv"])).view(n, H, dh)
+        o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
+                                           attn_mask=mask)
+        x = x + F.linear(o.transpose(0, 1).reshape(n, d), t(lw["wo"]))
+        h2 = F.rms_norm(x, (d,), weight=t(lw["ffn_norm"]), eps=shape.eps)
+        x = x + F.linear(F.silu(F.linear(h2, t(lw["wg"]))) * F.linear(h2, t(lw["wu"])), t(lw["wd"]))
+    hf = F.rms_norm(x, (d,), weight=t(w["final_norm"]), eps=shape.eps)
+    logits = F.linear(hf, t(w["lm_head"]))
+    logits[:, shape.mask_id] = -float("inf")
+    return logits.numpy()
+
+
+# ----------------------------------------------------------------------------
+# Operators: closed forms and special cases
+# ----------------------------------------------------------------------------
+
+
+def test_rmsnorm_constant_vector_is_gain():
+    g = np.linspace(0.5, 2.0, 16)
+    for c in (3.0, -0.25, 1e3):
+        out = oracle.rmsnorm(np.full((1, 16), c), g, 1e-5)
+        np.testing.assert_allclose(out[0], g * c / np.sqrt(c * c + 1e-5), rtol=1e-14)
+
+
+def test_rmsnorm_matches_torch():
+    rng = np.random.default_rng(0)
+    x, g = rng.normal(size=(5, 48)), rng.normal(size=48)
+    ref = F.rms_norm(torch.from_numpy(x), (48,), weight=torch.from_numpy(g), eps=1e-5).numpy()
+    np.testing.assert_allclose(oracle.rmsnorm(x, g, 1e-5), ref, rtol=1e-12, atol=1e-14)
+
+
+def test_rope_identity_at_position_zero():
+    u = np.random.default_rng(1).normal(size=(3, 2, 8))
+    np.testing.assert_array_equal(oracle.rope(u, np.zeros(3, np.int64), 10000.0), u)
+
+
+def test_rope_is_complex_rotation_and_relative():
+    rng = np.random.default_rng(2)
+    dh, base = 16, 10000.0
+    q, k = rng.normal(size=(1, 1, dh)), rng.normal(size=(1, 1, dh))
+    # complex form: z_j = u_j + i u_{j+dh/2} multiplied by exp(i * pos * base^(-2j/dh))
+    half = dh // 2
+    ang = 7 * base ** (-2.0 * np.arange(half) / dh)
+    z = (q[0, 0, :half] + 1j * q[0, 0, half:]) * np.exp(1j * ang)
+    r = oracle.rope(q, np.array([7]), base)[0, 0]
+    np.testing.assert_allclose(r, np.concatenate([z.real, z.imag]), rtol=1e-13, atol=1e-15)
+    # norm preserved, and q.k depends only on the position difference
+    assert np.isclose(np.linalg.norm(r), np.linalg.norm(q), rtol=1e-13)
+    d1 = np.sum(oracle.rope(q, np.array([11]), base) * oracle.rope(k, np.array([4]), base))
+    d2 = np.sum(oracle.rope(q, np.array([107]), base) * oracle.rope(k, np.array([100]), base))
+    assert np.isclose(d1, d2, rtol=1e-10)
+
+
+def test_attention_uniform_when_scores_vanish():
+    rng = np.random.default_rng(3)
+    V = rng.normal(size=(9, 2, 4))
+    q = np.zeros((3, 2, 4))
+    out = oracle.attend(q, rng.normal(size=(9, 2, 4)), V, np.array([9, 5, 1]))
+    np.testing.assert_allclose(out[0], V.mean(axis=0), rtol=1e-13)
+    np.testing.assert_allclose(out[1], V[:5].mean(axis=0), rtol=1e-13)
+    np.testing.assert_allclose(out[2], V[0], rtol=1e-13)
+
+
+def test_attention_matches_sdpa():
+    rng = np.random.default_rng(4)
+    n, T, H, dh = 4, 11, 3, 8
+    q, K, V = rng.normal(size=(n, H, dh)), rng.normal(size=(T, H, dh)), rng.normal(size=(T, H, dh))
+    limits = np.array([11, 7, 3, 1])
+    allowed = np.arange(T)[None, :] < limits[:, None]
+    ref = F.scaled_dot_product_attention(torch.from_numpy(q).transpose(0, 1),
+                                         torch.from_numpy(K).transpose(0, 1),
+                                         torch.from_numpy(V).transpose(0, 1),
+                                         attn_mask=torch.from_numpy(allowed)).transpose(0, 1).numpy()
+    np.testing.assert_allclose(oracle.attend(q, K, V, limits), ref, rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(oracle.attend_masked(q, K, V, allowed), ref, rtol=1e-11, atol=1e-13)
+
+
+def test_silu_closed_form():
+    z = np.array([-3.0, 0.0, 0.5, 10.0])
+    np.testing.assert_allclose(oracle.silu(z), z * scipy.special.expit(z), rtol=1e-14)
+
+
+def test_confidence_is_softmax_max_without_mask():
+    rng = np.random.default_rng(5)
+    logits = rng.normal(size=(6, 50)) * 2
+    logits[:, 49] = -np.inf
+    logits[2, 10] = logits[2, 3] = 100.0          # a tie: lowest id wins
+    ids, conf = oracle.confidence(logits)
+    p = scipy.special.softmax(logits, axis=-1)
+    assert np.all(ids != 49)
+    assert ids[2] == 3
+    np.testing.assert_array_equal(ids, np.argmax(p, axis=-1))
+    np.testing.assert_allclose(conf, p.max(axis=-1), rtol=1e-13)
+    np.testing.assert_allclose(p.sum(axis=-1), 1.0, rtol=1e-13)
+
+
+def test_planted_lm_head_row_forces_argmax():
+    sh = MICRO
+    model, _ = micro_model()
+    hf = oracle.rmsnorm(np.random.default_rng(6).normal(size=(1, sh.d_model)), model.final_norm, sh.eps)
+    alpha, t = 0.05, 17
+    model._lm = model._lm.copy()
+    model._lm[t] = alpha * hf[0]
+    logits = model.lm_logits(hf)
+    ids, conf = oracle.confidence(logits)
+    assert ids[0] == t
+    expect = 1.0 / np.sum(np.exp(np.delete(logits[0], sh.mask_id) - alpha * hf[0] @ hf[0]))
+    np.testing.assert_allclose(conf[0], expect, rtol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# The whole forward against the independent PyTorch reference
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("shape", [MICRO, synth.TINY.with_layers(1)], ids=["micro", "tiny1"])
+def test_step_matches_torch_reference(shape):
+    model, w = micro_model(shape)
+    P0, W = 24, 12
+    prompt = synth.prompt_ids(shape, P0)
+    kv = oracle.OracleKV(shape, P0 + W)
+    oracle.prefill(model, kv, prompt)
+    tok, mask = synth.window(shape, W, range(3, W))
+    out = oracle.denoise_step(model, kv, tok, mask)
+    seq = np.concatenate([prompt, oracle.input_ids(shape, tok, mask)])
+    allowed = oracle.block_causal_allowed(P0 + W, P0, shape.block, window_from=P0)
+    ref = torch_forward(shape, w, seq, allowed)[P0:]
+    fin = np.isfinite(ref)
+    np.testing.assert_array_equal(fin, np.isfinite(out.logits))
+    np.testing.assert_allclose(out.logits[fin], ref[fin], rtol=1e-9, atol=1e-11)
+
+
+def test_one_row_no_prefix_is_textbook_mlp_block():
+    """A single row attends only to itself, so attention returns v."""
+    sh = MICRO.with_layers(1)
+    model, w = micro_model(sh)
+    kv = oracle.OracleKV(sh, 4)
+    ids = np.array([5])
+    x, _ = oracle.forward_rows(model, kv, ids, np.array([0]), np.array([1]), lm_head=False)
+    lw = {k: synth.as_f32(v).astype(np.float64) for k, v in w["layers"][0].items()}
+    x0 = synth.as_f32(w["embed"])[5].astype(np.float64)
+    h = x0 / np.sqrt(np.mean(x0 ** 2) + sh.eps) * lw["attn_norm"]
+    x1 = x0 + lw["wo"] @ (lw["wv"] @ h)
+    h2 = x1 / np.sqrt(np.mean(x1 ** 2) + sh.eps) * lw["ffn_norm"]
+    g = lw["wg"] @ h2
+    x2 = x1 + lw["wd"] @ (g / (1 + np.exp(-g)) * (lw["wu"] @ h2))
+    np.testing.assert_allclose(x[0], x2, rtol=1e-12, atol=1e-14)
+
+
+# ----------------------------------------------------------------------------
+# Cache = brute-force recompute (block-causal), step = full forward
+# ----------------------------------------------------------------------------
+
+
+def _build_prefix(model, sh, P0, n_blocks, cap):
+    kv = oracle.OracleKV(sh, cap)
+    prompt = synth.prompt_ids(sh, P0)
+    oracle.prefill(model, kv, prompt)
+    blocks = []
+    for b in range(n_blocks):
+        blk = synth.uniform_ids(50 + b, 1, sh.block, sh.mask_id)
+        oracle.append_block(model, kv, blk)
+        blocks.append(blk)
+    return kv, np.concatenate([prompt] + blocks)
+
+
+def test_cached_prefix_equals_block_causal_recompute():
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv, seq = _build_prefix(model, sh, P0, 2, P0 + 2 * sh.block)
+    _, _, K, V = oracle.forward_full(model, seq, oracle.block_causal_allowed(len(seq), P0, sh.block))
+    np.testing.assert_allclose(kv.K[:, :len(seq)], K, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(kv.V[:, :len(seq)], V, rtol=1e-10, atol=1e-12)
+
+
+def test_block_mask_really_hides_the_future():
+    """Changing a later block must not change earlier cached rows."""
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv1, _ = _build_prefix(model, sh, P0, 1, P0 + 2 * sh.block)
+    kv2 = kv1.copy()
+    oracle.append_block(model, kv1, synth.uniform_ids(90, 1, sh.block, sh.mask_id))
+    oracle.append_block(model, kv2, synth.uniform_ids(91, 1, sh.block, sh.mask_id))
+    n = P0 + sh.block
+    np.testing.assert_array_equal(kv1.K[:, :n], kv2.K[:, :n])
+    assert not np.allclose(kv1.K[:, n:n + sh.block], kv2.K[:, n:n + sh.block])
+
+
+def test_step_with_speculative_window_equals_full_forward():
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv, seq = _build_prefix(model, sh, P0, 1, P0 + 3 * sh.block)
+    W = 2 * sh.block
+    tok, mask = synth.window(sh, W, list(range(24, 32)) + list(range(32, 64)))
+    out = oracle.denoise_step(model, kv, tok, mask)
+    full_seq = np.concatenate([seq, oracle.input_ids(sh, tok, mask)])
+    allowed = oracle.block_causal_allowed(len(full_seq), P0, sh.block, window_from=len(seq))
+    _, logits, _, _ = oracle.forward_full(model, full_seq, allowed)
+    np.testing.assert_allclose(out.logits[:, :-1], logits[len(seq):, :-1], rtol=1e-10, atol=1e-12)
+    assert kv.prefix_len == len(seq)            # a step never grows the prefix
+
+
+def test_window_permutation_permutes_outputs():
+    sh = MICRO
+    model, _ = micro_model(sh)
+    kv, seq = _build_prefix(model, sh, 16, 0, 16 + sh.block)
+    P = kv.prefix_len
+    ids = synth.uniform_ids(7, 1, sh.block, sh.vocab)
+    pos = P + np.arange(sh.block)
+    lim = np.full(sh.block, P + sh.block)
+    perm = np.random.default_rng(8).permutation(sh.block)
+    _, l1 = oracle.forward_rows(model, kv.copy(), ids, pos, lim, lm_head=True)
+    _, l2 = oracle.forward_rows(model, kv.copy(), ids[perm], pos[perm], lim, lm_head=True)
+    np.testing.assert_allclose(l2[:, :-1], l1[perm, :-1], rtol=1e-10, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# Refresh special cases
+# ----------------------------------------------------------------------------
+
+
+def test_refresh_with_unchanged_ids_is_noop():
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv, seq = _build_prefix(model, sh, P0, 2, P0 + 2 * sh.block)
+    before_K, before_V = kv.K.copy(), kv.V.copy()
+    pos = np.array([P0 + 3, P0 + 40, 5])
+    oracle.refresh(model, kv, pos, seq[pos], lm_head=False)
+    np.testing.assert_allclose(kv.K, before_K, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(kv.V, before_V, rtol=1e-10, atol=1e-12)
+
+
+def test_refresh_whole_last_block_equals_recompute():
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv, seq = _build_prefix(model, sh, P0, 2, P0 + 2 * sh.block)
+    last = np.arange(P0 + sh.block, P0 + 2 * sh.block)
+    new = synth.uniform_ids(77, 1, sh.block, sh.mask_id)
+    res = oracle.refresh(model, kv, last, new, lm_head=True)
+    seq2 = seq.copy()
+    seq2[last] = new
+    _, logits, K, V = oracle.forward_full(model, seq2, oracle.block_causal_allowed(len(seq2), P0, sh.block))
+    np.testing.assert_allclose(kv.K[:, :len(seq2)], K, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(kv.V[:, :len(seq2)], V, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(res[2][:, :-1], logits[last, :-1], rtol=1e-10, atol=1e-12)
+
+
+def test_refresh_is_sparse():
+    """Only the refreshed rows change; dependants keep their (stale) K/V."""
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv, seq = _build_prefix(model, sh, P0, 2, P0 + 2 * sh.block)
+    before = kv.K.copy()
+    pos = np.array([P0 + 1, P0 + 33])
+    oracle.refresh(model, kv, pos, np.array([1, 2]), lm_head=False)
+    other = np.setdiff1d(np.arange(kv.prefix_len), pos)
+    np.testing.assert_array_equal(kv.K[:, other], before[:, other])
+    assert not np.allclose(kv.K[:, pos], before[:, pos])
+
+
+# ----------------------------------------------------------------------------
+# Commit and the generation loop
+# ----------------------------------------------------------------------------
+
+
+def test_commit_brute_force_exchange_property():
+    rng = np.random.default_rng(9)
+    for trial in range(200):
+        n = int(rng.integers(1, 9))
+        conf = rng.choice([0.1, 0.2, 0.3, 0.5], size=n)      # many ties
+        mask = rng.integers(0, 2, size=n).astype(np.uint8)
+        k = int(rng.integers(0, n + 2))
+        tok = np.full(n, -1, np.int32)
+        pred = np.arange(100, 100 + n, dtype=np.int32)
+        m0 = mask.copy()
+        chosen = oracle.commit(conf, pred, tok, mask, 0, n, k)
+        masked = [p for p in range(n) if m0[p]]
+        assert len(chosen) == min(k, len(masked))
+        # brute force: the chosen set is the unique subset that beats every left-out candidate
+        best = None
+        for S in itertools.combinations(masked, len(chosen)):
+            rest = [q for q in masked if q not in S]
+            if all(conf[p] > conf[q] or (conf[p] == conf[q] and p < q) for p in S for q in rest):
+                assert best is None
+                best = set(S)
+        assert set(chosen.tolist()) == best
+        for p in chosen:
+            assert tok[p] == pred[p] and mask[p] == 0
+        assert np.all(mask[[q for q in range(n) if q not in chosen]] == m0[[q for q in range(n) if q not in chosen]])
+
+
+def test_commit_segment_only():
+    conf = np.array([0.9, 0.8, 0.7, 0.6])
+    mask = np.ones(4, np.uint8)
+    tok = np.zeros(4, np.int32)
+    chosen = oracle.commit(conf, np.arange(4, dtype=np.int32) + 10, tok, mask, 2, 2, 1)
+    assert chosen.tolist() == [2] and mask.tolist() == [1, 1, 0, 1]
+
+
+@pytest.mark.parametrize("n,s", [(32, 4), (32, 32), (24, 7), (5, 8)])
+def test_commit_schedule(n, s):
+    k = oracle.commit_schedule(n, s)
+    assert sum(k) == n and len(k) == s and max(k) - min(k) <= 1 and k == sorted(k, reverse=True)
+
+
+def test_tiny_generation_invariants():
+    """4 steps x top-8 over a 32-token all-MASK block (fp32 tiny model)."""
+    sh = synth.TINY
+    model, _ = micro_model(sh)
+    kv = oracle.OracleKV(sh, 64 + 32)
+    oracle.prefill(model, kv, synth.prompt_ids(sh, 64))
+    tok, mask = synth.window(sh, 32, range(32))
+    committed = {}
+    for step, k in enumerate(oracle.commit_schedule(32, 4)):
+        out = oracle.denoise_step(model, kv, tok, mask)
+        p = scipy.special.softmax(out.logits, axis=-1)
+        np.testing.assert_allclose(p.sum(axis=-1), 1.0, rtol=1e-12)
+        np.testing.assert_allclose(out.conf, p.max(axis=-1), rtol=1e-12)
+        assert np.all(out.ids != sh.mask_id)
+        n_before = int(mask.sum())
+        chosen = oracle.commit(out.conf, out.ids, tok, mask, 0, 32, k)
+        assert len(chosen) == min(k, n_before) == 8
+        for pos, t in committed.items():            # never re-masked, never changed
+            assert mask[pos] == 0 and tok[pos] == t
+        for pos in chosen:
+            committed[int(pos)] = int(tok[pos])
+        assert kv.prefix_len == 64
+    assert mask.sum() == 0 and np.all(tok != sh.mask_id)
+
+
+# ----------------------------------------------------------------------------
+# int8 quantisation
+# ----------------------------------------------------------------------------
+
+
+def test_int8_quantiser_bounds():
+    w = synth.as_f32(synth.weight(MICRO, "wg", 0, "bf16"))
+    w[3] = 0.0
+    q, s = oracle.quantize_rows_int8(w)
+    assert q.dtype == np.int8 and s.dtype == np.float32
+    assert np.all(np.abs(q.astype(int)) <= 127)
+    nz = s > 0
+    assert np.all(np.abs(q[nz]).max(axis=1) == 127)              # each row's extreme maps to 127
+    assert np.all(q[3] == 0) and s[3] == 0
+    err = np.abs(w.astype(np.float64) - oracle.dequantize_rows(q, s))
+    assert np.all(err <= s[:, None].astype(np.float64) * (0.5 + 2e-5))   # w / s is itself rounded in float32
+    np.testing.assert_array_equal(s[nz], np.abs(w[nz]).max(axis=1) / np.float32(127))
+
+
+def test_int8_model_is_bf16_model_with_dequantised_weights():
+    sh = MICRO
+    w = synth.all_weights(sh, "bf16", 0)
+    m8 = oracle.OracleModel(sh, w, int8=True)
+    wd = dict(w)
+    wd["lm_head"] = oracle.dequantize_rows(*oracle.quantize_rows_int8(synth.as_f32(w["lm_head"])))
+    wd["layers"] = []
+    for lw in w["layers"]:
+        d = dict(lw)
+        for k in om.GEMM_WEIGHTS:
+            d[k] = oracle.dequantize_rows(*oracle.quantize_rows_int8(synth.as_f32(lw[k])))
+        wd["layers"].append(d)
+    mref = oracle.OracleModel(sh, wd)
+    for m in (m8, mref):
+        kv = oracle.OracleKV(sh, 40)
+        oracle.prefill(m, kv, synth.prompt_ids(sh, 8))
+        m.out = oracle.denoise_step(m, kv, *synth.window(sh, 32, range(32))).logits
+    np.testing.assert_array_equal(m8.out, mref.out)
+
+
+def test_synth_inputs_are_reproducible_and_sliceable():
+    a = synth.normal(0, 5, 1000, "bf16")
+    b = synth.normal(0, 5, 101, "bf16", offset=333)
+    np.testing.assert_array_equal(a[333:434], b)
+    f = synth.as_f32(synth.normal(0, 6, 200000, "bf16"))
+    assert abs(f.std() - 0.02) < 2e-4 and abs(f.mean()) < 2e-4
+    ids = synth.prompt_ids(synth.TINY, 5000)
+    assert ids.min() >= 0 and ids.max() < synth.TINY.mask_id
