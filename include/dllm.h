@@ -1,0 +1,235 @@
+/*
+ * dllm.h - C ABI of the MI355X (gfx950) denoising-step library (libdllm.so).
+ *
+ * Block-wise diffusion-LLM inference (paper: Background, "Block-Wise Decoding"):
+ * the output is split into consecutive blocks decoded left to right.  At each
+ * denoising step the transformer runs over the current decoding window (the
+ * current block, optionally extended with speculative draft tokens of the next
+ * block; System Design, "Multi-Block Speculative Decoding"), attending to a
+ * reused prefix KV cache and globally within the window, and every masked
+ * position gets a predicted id and a confidence; a confidence-selected subset is
+ * committed.  Completed blocks are appended to the prefix cache; revised prefix
+ * positions can have their KV refreshed sparsely (System Design, "Dual-Path
+ * Progressive Revision", "Sparse Cache Refresh"), visible from the next step on.
+ *
+ * Model: pre-norm LLaMA-style blocks (RMSNorm, multi-head attention with
+ * rotate-half RoPE, SwiGLU FFN, no biases) and an untied LM head, as the paper's
+ * operator list (RMSNorm, matrix multiplication, FlashAttention, elementwise ops;
+ * Implementation section) and the LLaDA-8B model it evaluates imply.
+ *
+ * Conventions
+ *  - Every function returns an int status: DLLM_OK (0) or a negative DLLM_E_*.
+ *    dllm_last_error() returns a thread-local message for the last failure.
+ *    No C++ exception crosses this boundary.
+ *  - Arguments are validated on the host before any GPU work is queued; a call
+ *    that fails validation queues nothing and changes no state.
+ *  - Device work is asynchronous on the given stream (a hipStream_t; NULL is
+ *    the null stream).  Outputs are valid once that stream has completed.
+ *    The host-side prefix length of a KV handle changes when the call returns.
+ *  - "d_" pointers are device pointers; the caller owns them and they must stay
+ *    valid until the stream work that uses them has finished.  The library owns
+ *    only its handles, its prepacked weight copy and its workspaces, all freed by
+ *    the matching *_destroy call.
+ *  - A model handle is not thread-safe: calls that use one model must not run
+ *    concurrently (they share the model's workspaces), and all its calls should
+ *    be issued on one stream, or on streams the caller orders.
+ *
+ * Readings where the paper is silent (also fixed by the test oracle):
+ *  - confidence = softmax probability of the argmax token (temperature 0); the
+ *    MASK id is excluded from argmax and softmax; argmax ties -> lowest id;
+ *  - commit order: higher confidence first, equal confidence -> lower position;
+ *  - the prefix is block-causal: the prompt is one bidirectional block, block b
+ *    sees blocks <= b; a denoising window sees every key in [0, P + W).
+ */
+#ifndef DLLM_H
+#define DLLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DLLM_OK 0
+#define DLLM_E_INVAL (-1)     /* bad argument (null pointer, out-of-range size, ...) */
+#define DLLM_E_CAPACITY (-2)  /* the KV cache or a window limit would overflow */
+#define DLLM_E_DTYPE (-3)     /* unsupported dtype / shape combination */
+#define DLLM_E_HIP (-4)       /* a HIP runtime call failed */
+#define DLLM_E_UNIMPL (-5)    /* not implemented for this configuration */
+#define DLLM_E_NOMEM (-6)     /* device allocation failed */
+
+/* Weight / arithmetic types. */
+#define DLLM_F32 0   /* fp32 weights, fp32 activations and KV cache */
+#define DLLM_BF16 1  /* bf16 weights, bf16 GEMM operands and KV cache, fp32 accumulate */
+#define DLLM_W8 2    /* int8 weights with fp32 per-output-row scales, bf16 activations */
+
+typedef struct dllm_model dllm_model;
+typedef struct dllm_kv dllm_kv;
+typedef void* dllm_stream; /* hipStream_t */
+
+typedef struct dllm_config {
+    int32_t n_layers;
+    int32_t d_model;     /* = n_heads * head_dim */
+    int32_t n_heads;
+    int32_t head_dim;    /* 64 or 128 */
+    int32_t d_ff;        /* SwiGLU hidden size */
+    int32_t vocab;
+    int32_t mask_id;     /* id of the MASK token, 0 <= mask_id < vocab */
+    int32_t block;       /* block size of the block-causal prefix (32) */
+    float eps;           /* RMSNorm epsilon */
+    float rope_base;     /* RoPE base (10000) */
+    int32_t dtype;       /* DLLM_F32, DLLM_BF16 or DLLM_W8 */
+    int32_t max_window;  /* largest row count of a step / append / refresh call (<= 256) */
+    int32_t max_pos;     /* positions covered by the RoPE table; bounds every KV capacity */
+} dllm_config;
+
+/* Device pointers to row-major [out][in] matrices of one layer.
+ * DLLM_F32: float; DLLM_BF16 and DLLM_W8: bfloat16 (W8 quantises them on create).
+ * wq, wk, wv, wo: [d][d]; wg, wu: [d_ff][d]; wd: [d][d_ff]; norms: float [d]. */
+typedef struct dllm_layer_weights {
+    const void* wq;
+    const void* wk;
+    const void* wv;
+    const void* wo;
+    const void* wg;
+    const void* wu;
+    const void* wd;
+    const float* attn_norm;
+    const float* ffn_norm;
+} dllm_layer_weights;
+
+typedef struct dllm_weights {
+    const void* embed;                 /* [vocab][d]: float (F32) or bfloat16 (BF16, W8) */
+    const void* lm_head;               /* [vocab][d], same type as the layer matrices */
+    const float* final_norm;           /* [d] */
+    const dllm_layer_weights* layers;  /* HOST array of n_layers entries */
+} dllm_weights;
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* dllm_last_error(void);
+
+/* Library version string. */
+const char* dllm_version(void);
+
+/* Creates a model: validates the config, allocates the library's own copy of the
+ * weights prepacked into MFMA-fragment order (and, for DLLM_W8, quantises every
+ * matrix except the embedding to int8 with per-output-row fp32 scales
+ * s = max|w| / 127, q = round-half-even(w / s), decided in fp32), builds the
+ * RoPE table, and allocates workspaces for max_window rows.  The caller's weight
+ * buffers are only read during this call (on `stream`, which is synchronised
+ * before returning) and may be freed afterwards.  Quantisation is the analog of
+ * the paper's converter layout pass (Implementation section). */
+int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream stream,
+                      dllm_model** out);
+int dllm_model_destroy(dllm_model* m);
+
+/* Bytes of device memory a KV cache of `capacity` positions needs.
+ * Layout inside the caller's buffer, element type float (F32) or bfloat16:
+ *   K   of layer l, head h, position p, dim j: ((l*2+0)*H + h)*cap*Dh + p*Dh + j
+ *   V^T of layer l, head h, dim j, position p: ((l*2+1)*H + h)*Dh*cap + j*cap + p
+ * K is stored after RoPE. */
+int dllm_kv_bytes(const dllm_model* m, int32_t capacity, size_t* bytes);
+
+/* Wraps a caller-owned device buffer of at least dllm_kv_bytes() bytes as a KV
+ * cache (borrowed, not freed by the library).  prefix_len starts at 0.
+ * capacity must be <= cfg.max_pos. */
+int dllm_kv_create(const dllm_model* m, void* d_buf, size_t bytes, int32_t capacity, dllm_kv** out);
+int dllm_kv_destroy(dllm_kv* kv);
+int dllm_kv_prefix_len(const dllm_kv* kv, int32_t* prefix_len, int32_t* prompt_len);
+/* Rewinds (or restores) the prefix length, e.g. to repeat an identical step.
+ * Requires prompt_len <= prefix_len <= capacity; rows past it are ignored. */
+int dllm_kv_set_prefix_len(dllm_kv* kv, int32_t prefix_len);
+
+/* Prompt processing (Evaluation setup: latency includes prompt processing).
+ * Runs the n prompt ids through every layer as one bidirectional block at
+ * positions [0, n) and writes their K/V.  Requires prefix_len == 0; sets
+ * prefix_len = prompt_len = n.  E_CAPACITY if n > capacity.  Ids outside
+ * [0, vocab) are read as the MASK id. */
+int dllm_prefill(dllm_model* m, dllm_kv* kv, const int32_t* d_ids, int32_t n, dllm_stream stream);
+
+/* One denoising step over the W-row window at positions [P, P + W), P = prefix_len
+ * (Background, "Block-Wise Decoding"; System Design, "Multi-Block Speculative
+ * Decoding").  Row i feeds the MASK id if d_mask[i] != 0, else d_tok[i]; every
+ * row attends to all keys [0, P + W) (the whole prefix and the window, both
+ * directions).  Writes, for every row, the argmax id (MASK excluded, lowest id on
+ * ties) to d_out_id[W] and its softmax probability to d_out_conf[W].  Logits never
+ * reach device memory.  The window's K/V are written to cache rows [P, P + W),
+ * which stay scratch (prefix_len is unchanged), so draft rows never enter the
+ * prefix.  E_INVAL if W < 1 or W > max_window; E_CAPACITY if P + W > capacity. */
+int dllm_denoise_step(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask,
+                      int32_t W, int32_t* d_out_id, float* d_out_conf, dllm_stream stream);
+
+/* Confidence-selected commit over one segment (Background: "updates a
+ * confidence-selected subset"; a draft segment is committed separately, System
+ * Design, "Multi-Block Speculative Decoding").  Among the positions p in
+ * [seg_begin, seg_begin + seg_len) with d_mask[p] != 0, takes the k with the
+ * highest d_conf (ties -> lower position), sets d_tok[p] = d_id[p] and
+ * d_mask[p] = 0.  Writes the committed positions, in that order, to
+ * d_committed_pos[0 .. n) and n = min(k, #masked) to *d_n_committed.
+ * d_committed_pos must hold min(k, seg_len) entries; it and d_n_committed may be
+ * NULL.  E_INVAL if k < 0, seg_begin < 0, seg_len < 0 or seg_len > 1024. */
+int dllm_commit(const float* d_conf, const int32_t* d_id, int32_t* d_tok, uint8_t* d_mask,
+                int32_t seg_begin, int32_t seg_len, int32_t k, int32_t* d_committed_pos,
+                int32_t* d_n_committed, dllm_stream stream);
+
+/* Appends a completed block (Background, "Block-Wise Decoding": completed blocks
+ * are reused through the KV cache).  Its n ids run through every layer at
+ * positions [P, P + n), attending to keys [0, P + n); their K/V are written and
+ * prefix_len becomes P + n.  The ids must hold no MASK.  E_INVAL if n < 1 or
+ * n > max_window; E_CAPACITY if P + n > capacity. */
+int dllm_append_prefix_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_block_tok, int32_t n,
+                          dllm_stream stream);
+
+/* Sparse KV refresh of revised prefix positions (System Design, "Sparse Cache
+ * Refresh": confidence, identity and KV of revisable tokens are recomputed and
+ * merged at a step boundary).  Each of the n rows runs its new id d_new_id[i] at
+ * position d_pos[i]; at every layer the new K/V of all n rows replace the cached
+ * ones before that layer's attention, and row i attends to keys [0, e_i), e_i the
+ * end of its block (prompt: prompt_len; else prompt_len + block * (1 + (p -
+ * prompt_len) / block)), capped at prefix_len.  Every other cached row is left as
+ * it was.  If d_out_id / d_out_conf are non-NULL, also writes the rows' argmax id
+ * and confidence.  The positions are copied to the host (the call synchronises
+ * `stream`) to validate them: E_INVAL unless all are distinct and < prefix_len,
+ * n >= 1 and n <= max_window. */
+int dllm_refresh_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_pos, const int32_t* d_new_id,
+                    int32_t n, int32_t* d_out_id, float* d_out_conf, dllm_stream stream);
+
+/* Parity only (never on the timed path): the same step as dllm_denoise_step, also
+ * writing the full logits d_logits[W][vocab] (float, MASK column = -inf).  If
+ * d_out_id / d_out_conf are non-NULL they receive the step's outputs. */
+int dllm_debug_logits(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask,
+                      int32_t W, float* d_logits, int32_t* d_out_id, float* d_out_conf,
+                      dllm_stream stream);
+
+/* Parity only: runs the window through the first n_layers layers (0 = embedding
+ * only) and copies the fp32 residual stream to d_x[W][d_model]. */
+int dllm_debug_hidden(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask,
+                      int32_t W, int32_t n_layers, float* d_x, dllm_stream stream);
+
+/* Kernel timing probe.  Kernel classes: */
+#define DLLM_K_QKV 0
+#define DLLM_K_ATTN 1
+#define DLLM_K_OPROJ 2
+#define DLLM_K_GATEUP 3
+#define DLLM_K_DOWN 4
+#define DLLM_K_LMHEAD 5
+/* While enabled, every launch of `kernel_class` (at most max_records of them) is
+ * bracketed by HIP events recorded on the launch stream.  kernel_class < 0
+ * disables.  Recording the events adds small gaps, so timed throughput runs
+ * should leave the probe disabled. */
+int dllm_probe_enable(dllm_model* m, int32_t kernel_class, int32_t max_records);
+/* Synchronises the recorded events and returns the count and mean duration
+ * (milliseconds) of the recorded launches; resets the record count. */
+int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms);
+
+/* Algorithmic bytes one launch of a kernel class moves for a window of W rows at
+ * prefix P (weights once, KV read, KV written, activations; no logits).  Used to
+ * express achieved bandwidth. */
+int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DLLM_H */

@@ -1,0 +1,124 @@
+// Shared device helpers for the gfx950 denoising-step kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+
+namespace dllm {
+
+// Weight element types of the packed GEMM operand.
+enum WType : int { WT_F32 = 0, WT_BF16 = 1, WT_I8 = 2 };
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) { return bf16_to_f32(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { return f32_to_bf16(v); }
+
+// ---------------------------------------------------------------------------
+// MFMA operand fragments (gfx950, wave64)
+//
+// v_mfma_f32_16x16x32_bf16: lane l (g = l / 16) holds A[l % 16][8g .. 8g+7] and
+// B[8g .. 8g+7][l % 16]; the result lane l holds D[4g + i][l % 16], i = 0..3.
+// v_mfma_f32_16x16x4_f32:   lane l holds A[l % 16][g] and B[g][l % 16].
+//
+// A "chunk" is 16 rows x KC columns stored as 64 lanes x 16 bytes (1 KiB):
+//   bf16 (KC = 32): lane l bytes = row l%16, cols 8g .. 8g+7
+//   f32  (KC = 16): lane l float s = row l%16, col 4s + g (s = 0..3, one MFMA each)
+//   int8 (KC = 64): lane l byte 8h + e = row l%16, col 32h + 8g + e (h = 0..1)
+// Packed weights: chunk (nt, kc) at byte ((nt * KCn + kc) * 64 + lane) * 16.
+// Activation fragments use the same chunk shape with rows = tokens; their chunk
+// width is 32 (bf16) or 16 (f32) columns:
+//   chunk (mt, kcx) at byte ((mt * KCx + kcx) * 64 + lane) * 16.
+// ---------------------------------------------------------------------------
+
+template <int WT> struct WTraits;
+template <> struct WTraits<WT_F32> { static constexpr int KC = 16; static constexpr int XPER = 1; };
+template <> struct WTraits<WT_BF16> { static constexpr int KC = 32; static constexpr int XPER = 1; };
+template <> struct WTraits<WT_I8> { static constexpr int KC = 64; static constexpr int XPER = 2; };
+
+// Columns per activation chunk: 16 for fp32 activations, 32 for bf16.
+template <int WT> struct XCols { static constexpr int v = (WT == WT_F32) ? 16 : 32; };
+
+// Byte offset of activation element (m, k) in the fragment buffer with KCx chunks per tile row.
+template <bool F32>
+__device__ __forceinline__ size_t xfrag_offset(int m, int k, int KCx) {
+    const int mt = m >> 4, r = m & 15;
+    if (F32) {
+        const int kc = k >> 4, kk = k & 15;
+        const int g = kk & 3, s = kk >> 2;
+        return ((size_t)(mt * KCx + kc) * 64 + (r + 16 * g)) * 16 + s * 4;
+    } else {
+        const int kc = k >> 5, kk = k & 31;
+        const int g = kk >> 3, e = kk & 7;
+        return ((size_t)(mt * KCx + kc) * 64 + (r + 16 * g)) * 16 + e * 2;
+    }
+}
+
+template <bool F32>
+__device__ __forceinline__ void xfrag_store(void* base, int m, int k, int KCx, float v) {
+    char* p = (char*)base + xfrag_offset<F32>(m, k, KCx);
+    if (F32) *(float*)p = v;
+    else *(uint16_t*)p = f32_to_bf16(v);
+}
+
+__device__ __forceinline__ f32x4_t mfma_bf16(const u32x4_t& a, const u32x4_t& b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4_t mfma_f32(float a, float b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// 8 signed bytes (two dwords) -> 8 bf16 (exact: |q| <= 127 fits the 8-bit significand).
+__device__ __forceinline__ u32x4_t i8x8_to_bf16x8(uint32_t lo, uint32_t hi) {
+    u32x4_t r;
+    uint32_t w[2] = {lo, hi};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int b0 = (int)(int8_t)((w[j] >> (16 * p)) & 0xFF);
+            const int b1 = (int)(int8_t)((w[j] >> (16 * p + 8)) & 0xFF);
+            const uint32_t f0 = __float_as_uint((float)b0) >> 16;
+            const uint32_t f1 = __float_as_uint((float)b1) >> 16;
+            r[2 * j + p] = f0 | (f1 << 16);
+        }
+    }
+    return r;
+}
+
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ float warp_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ u32x4_t ldg16(const void* p) { return *(const u32x4_t*)p; }
+__device__ __forceinline__ u32x4_t ldg16_nt(const void* p) {
+    return __builtin_nontemporal_load((const u32x4_t*)p);
+}
+
+}  // namespace dllm

@@ -1,0 +1,791 @@
+// libdllm: host runtime and C ABI of the gfx950 denoising-step library.
+//
+// One denoising step (a window of W <= 64 rows over a prefix cache) is, per
+// layer: fused RMSNorm+QKV+RoPE GEMM (K/V straight into the cache), window-vs-
+// prefix attention (+ split merge), O projection + residual, fused
+// RMSNorm+gate/up+SwiGLU GEMM, down projection + residual; then the final norm +
+// LM head fused with the (max, argmax, sum exp) reduction and its merge.  Every
+// launch is on the caller's stream; nothing is synchronised on the step path.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/dllm.h"
+#include "attention.hpp"
+#include "common.hpp"
+#include "gemm.hpp"
+#include "kernels.hpp"
+
+using namespace dllm;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+    g_last_error = msg;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                           \
+    do {                                                                                        \
+        hipError_t _e = (expr);                                                                 \
+        if (_e != hipSuccess)                                                                   \
+            return fail(DLLM_E_HIP, std::string(#expr) + ": " + hipGetErrorString(_e));        \
+    } while (0)
+
+inline int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+inline long round_up(long a, long b) { return (a + b - 1) / b * b; }
+
+// One packed GEMM operand.
+struct PackedW {
+    void* w = nullptr;      // chunks
+    float* scale = nullptr; // per packed row (int8) or nullptr
+    int N = 0;              // real rows
+    int K = 0;              // real columns
+    int n_tiles = 0;
+    int KCw = 0;
+    size_t bytes = 0;
+};
+
+struct LayerW {
+    PackedW qkv, o, gu, down;
+    float* g1 = nullptr;
+    float* g2 = nullptr;
+};
+
+struct Workspace {
+    int rows = 0;            // token rows (multiple of 64)
+    int wrows = 0;           // window rows for LM / attention partials (multiple of 64)
+    float* x = nullptr;      // [rows][d]
+    void* xg = nullptr;      // fragments, K = d
+    void* q = nullptr;       // [rows][d] act type
+    void* of = nullptr;      // fragments, K = d (attention output)
+    void* af = nullptr;      // fragments, K = d_ff
+    float* ssq = nullptr;    // [n_part_max][rows]
+    int* pos = nullptr;      // [rows]
+    int* lim = nullptr;      // [rows]
+    LmPartial* lm = nullptr; // [n_lm_wg][wrows]
+    float* opart = nullptr;  // [MAX_SPLIT][wrows][H][Dh]
+    float* mlpart = nullptr; // [MAX_SPLIT][wrows][H][2]
+};
+
+constexpr int MAX_SPLIT = 16;
+
+}  // namespace
+
+struct dllm_model {
+    dllm_config cfg;
+    int wt = 0;              // WT_F32 / WT_BF16 / WT_I8
+    bool xf32 = false;       // activations in fp32
+    size_t act_size = 2;     // bytes of one activation / KV element
+    int KCx_d = 0, KCx_f = 0;
+    std::vector<LayerW> layers;
+    PackedW lm;
+    void* embed = nullptr;
+    float* gf = nullptr;
+    float2* rope = nullptr;
+    void* wpool = nullptr;   // packed weights of every matrix
+    float* spool = nullptr;  // int8 scales
+    float* gpool = nullptr;  // norm gains
+    Workspace ws;
+    int n_part_max = 1;
+    int n_lm_wg = 1;
+    // probe
+    int probe_class = -1;
+    int probe_max = 0;
+    int probe_n = 0;
+    std::vector<hipEvent_t> ev_b, ev_e;
+};
+
+struct dllm_kv {
+    const dllm_model* model;
+    void* buf;
+    size_t bytes;
+    int capacity;
+    int Cs;
+    int prefix_len;
+    int prompt_len;
+};
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Launch configuration of the weight-streaming GEMMs
+// ---------------------------------------------------------------------------
+
+enum GemmKind { G_QKV = 0, G_RES = 1, G_GU = 2, G_LM = 3 };
+
+// Row tiles per workgroup: enough workgroups to cover 256 CUs, and few enough
+// registers that a 64-token tile does not spill.
+int pick_F(GemmKind k, int n_tiles, int MT) {
+    switch (k) {
+        case G_QKV: return n_tiles >= 256 * 3 ? 3 : 1;
+        case G_GU: return n_tiles >= 256 * 6 ? 6 : 1;
+        case G_LM:
+            if (n_tiles >= 256 * 8) return MT >= 4 ? 4 : 8;
+            return 1;
+        default: return 1;
+    }
+}
+
+int pick_MT(int M) {
+    if (M <= 16) return 1;
+    if (M <= 32) return 2;
+    return 4;
+}
+
+template <int WT, int F, int MT, int NW, int D, bool RSTD, class Epi>
+void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
+    hipLaunchKernelGGL((gemm_kernel<WT, F, MT, NW, D, RSTD, Epi>), dim3(gx, gy), dim3((NW + (RSTD ? 1 : 0)) * 64),
+                       0, s, g, epi);
+}
+
+template <int WT, int F, int NW, int D, bool RSTD, class Epi>
+int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
+    switch (MT) {
+        case 1: launch_gemm_inst<WT, F, 1, NW, D, RSTD>(g, epi, gx, gy, s); break;
+        case 2: launch_gemm_inst<WT, F, 2, NW, D, RSTD>(g, epi, gx, gy, s); break;
+        case 4: launch_gemm_inst<WT, F, 4, NW, D, RSTD>(g, epi, gx, gy, s); break;
+        default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
+    }
+    return DLLM_OK;
+}
+
+template <int WT, GemmKind KIND, class Epi>
+int launch_gemm(int F, int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
+    if constexpr (KIND == G_QKV) {
+        if (F == 3) return launch_gemm_mt<WT, 3, 4, 4, true>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 4, 8, true>(MT, g, epi, gx, gy, s);
+    } else if constexpr (KIND == G_GU) {
+        if (F == 6) return launch_gemm_mt<WT, 6, 4, 2, true>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 4, 8, true>(MT, g, epi, gx, gy, s);
+    } else if constexpr (KIND == G_LM) {
+        if (F == 8) return launch_gemm_mt<WT, 8, 4, 2, true>(MT, g, epi, gx, gy, s);
+        if (F == 4) return launch_gemm_mt<WT, 4, 4, 2, true>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 4, 8, true>(MT, g, epi, gx, gy, s);
+    } else {
+        return launch_gemm_mt<WT, 1, 8, 8, false>(MT, g, epi, gx, gy, s);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Probe
+// ---------------------------------------------------------------------------
+
+struct ProbeScope {
+    dllm_model* m;
+    hipStream_t s;
+    bool on;
+    ProbeScope(dllm_model* m_, int cls, hipStream_t s_) : m(m_), s(s_) {
+        on = (m->probe_class == cls && m->probe_n < m->probe_max);
+        if (on) (void)hipEventRecord(m->ev_b[m->probe_n], s);
+    }
+    ~ProbeScope() {
+        if (on) {
+            (void)hipEventRecord(m->ev_e[m->probe_n], s);
+            ++m->probe_n;
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Workspace
+// ---------------------------------------------------------------------------
+
+void free_ws(Workspace& w) {
+    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.ssq, w.pos, w.lim, w.lm, w.opart, w.mlpart};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    w = Workspace{};
+}
+
+int alloc_zero(void** p, size_t bytes) {
+    if (hipMalloc(p, std::max<size_t>(bytes, 256)) != hipSuccess) {
+        *p = nullptr;
+        return fail(DLLM_E_NOMEM, "device allocation of " + std::to_string(bytes) + " bytes failed");
+    }
+    HIP_TRY(hipMemset(*p, 0, std::max<size_t>(bytes, 256)));
+    return DLLM_OK;
+}
+
+int ensure_ws(dllm_model* m, int rows_needed) {
+    const dllm_config& c = m->cfg;
+    const int rows = (int)round_up(std::max(rows_needed, 1), 64);
+    if (m->ws.rows >= rows && m->ws.x) return DLLM_OK;
+    HIP_TRY(hipDeviceSynchronize());
+    free_ws(m->ws);
+    Workspace& w = m->ws;
+    w.rows = rows;
+    w.wrows = (int)round_up(c.max_window, 64);
+    const size_t d = c.d_model;
+    int rc;
+#define ALLOC(ptr, bytes) \
+    if ((rc = alloc_zero((void**)&(ptr), (bytes))) != DLLM_OK) { free_ws(w); return rc; }
+    ALLOC(w.x, (size_t)rows * d * 4);
+    ALLOC(w.xg, (size_t)(rows / 16) * m->KCx_d * 1024);
+    ALLOC(w.q, (size_t)rows * d * m->act_size);
+    ALLOC(w.of, (size_t)(rows / 16) * m->KCx_d * 1024);
+    ALLOC(w.af, (size_t)(rows / 16) * m->KCx_f * 1024);
+    ALLOC(w.ssq, (size_t)m->n_part_max * rows * 4);
+    ALLOC(w.pos, (size_t)rows * 4);
+    ALLOC(w.lim, (size_t)rows * 4);
+    ALLOC(w.lm, (size_t)m->n_lm_wg * w.wrows * sizeof(LmPartial));
+    ALLOC(w.opart, (size_t)MAX_SPLIT * w.wrows * d * 4);
+    ALLOC(w.mlpart, (size_t)MAX_SPLIT * w.wrows * c.n_heads * 2 * 4);
+#undef ALLOC
+    return DLLM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Weight prepacking
+// ---------------------------------------------------------------------------
+
+int kc_of(int wt) { return wt == WT_F32 ? 16 : (wt == WT_BF16 ? 32 : 64); }
+
+void plan_packed(PackedW& p, int wt, int N, int K) {
+    p.N = N;
+    p.K = K;
+    p.n_tiles = ceil_div(N, 16);
+    p.KCw = ceil_div(K, kc_of(wt));
+    p.bytes = (size_t)p.n_tiles * p.KCw * 1024;
+}
+
+template <typename ST>
+int pack_one(dllm_model* m, PackedW& p, const PackSrc& src, hipStream_t s) {
+    const size_t units = (size_t)p.n_tiles * p.KCw * 64;
+    const int blocks = ceil_div((long)units, 256);
+    if (m->wt == WT_I8) {
+        hipLaunchKernelGGL((row_scale_kernel<ST>), dim3(p.n_tiles * 16), dim3(256), 0, s, src, p.n_tiles * 16, p.scale);
+        hipLaunchKernelGGL((pack_kernel<WT_I8, ST>), dim3(blocks), dim3(256), 0, s, src, p.n_tiles, p.KCw,
+                           (u32x4_t*)p.w, (const float*)p.scale);
+    } else if (m->wt == WT_BF16) {
+        hipLaunchKernelGGL((pack_kernel<WT_BF16, ST>), dim3(blocks), dim3(256), 0, s, src, p.n_tiles, p.KCw,
+                           (u32x4_t*)p.w, (const float*)nullptr);
+    } else {
+        hipLaunchKernelGGL((pack_kernel<WT_F32, ST>), dim3(blocks), dim3(256), 0, s, src, p.n_tiles, p.KCw,
+                           (u32x4_t*)p.w, (const float*)nullptr);
+    }
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
+int validate_config(const dllm_config* c) {
+    if (!c) return fail(DLLM_E_INVAL, "config is NULL");
+    if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->head_dim < 1 || c->d_ff < 1 || c->vocab < 2)
+        return fail(DLLM_E_INVAL, "shape fields must be positive (vocab >= 2)");
+    if (c->n_heads * c->head_dim != c->d_model) return fail(DLLM_E_INVAL, "d_model != n_heads * head_dim");
+    if (c->mask_id < 0 || c->mask_id >= c->vocab) return fail(DLLM_E_INVAL, "mask_id out of range");
+    if (c->block < 1) return fail(DLLM_E_INVAL, "block must be >= 1");
+    if (c->max_window < 1 || c->max_window > 256) return fail(DLLM_E_INVAL, "max_window must be in [1, 256]");
+    if (c->max_pos < 1) return fail(DLLM_E_INVAL, "max_pos must be >= 1");
+    if (!(c->eps > 0.f) || !(c->rope_base > 1.f)) return fail(DLLM_E_INVAL, "eps must be > 0 and rope_base > 1");
+    if (c->dtype != DLLM_F32 && c->dtype != DLLM_BF16 && c->dtype != DLLM_W8)
+        return fail(DLLM_E_DTYPE, "dtype must be DLLM_F32, DLLM_BF16 or DLLM_W8");
+    if (c->dtype == DLLM_F32) {
+        if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
+            return fail(DLLM_E_DTYPE, "fp32 models need head_dim 32, 64 or 128");
+    } else if (c->head_dim != 64 && c->head_dim != 128) {
+        return fail(DLLM_E_DTYPE, "bf16 / int8 models need head_dim 64 or 128");
+    }
+    if (c->d_model % 32 != 0) return fail(DLLM_E_DTYPE, "d_model must be a multiple of 32");
+    if (c->d_ff % 8 != 0) return fail(DLLM_E_DTYPE, "d_ff must be a multiple of 8");
+    return DLLM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The forward over a set of rows
+// ---------------------------------------------------------------------------
+
+struct FwdArgs {
+    int M;                    // rows
+    const int* tok;           // ids
+    const uint8_t* mask;      // nullable
+    int pos_base;             // row m at pos_base + m unless pos
+    const int* pos;           // device positions or nullptr
+    int T;                    // key count for rows without own limit
+    const int* lim;           // per-row limits or nullptr
+    int n_layers;             // layers to run
+    bool lm;
+    float* logits;            // debug logits or nullptr
+    int* out_id;
+    float* out_conf;
+    float* xout;              // residual copy or nullptr
+};
+
+template <int WT, typename AT>
+int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
+    constexpr bool XF32 = (WT == WT_F32);
+    const dllm_config& c = m->cfg;
+    const int d = c.d_model, H = c.n_heads, Dh = c.head_dim;
+    int rc = ensure_ws(m, a.M);
+    if (rc) return rc;
+    Workspace& w = m->ws;
+
+    int MT, gy;
+    if (a.M <= 64) { MT = pick_MT(a.M); gy = 1; }
+    else { MT = 4; gy = ceil_div(a.M, 64); }
+    const int Mc = gy * MT * 16;    // rows computed (padded)
+
+    hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(256), 0, s, (const AT*)m->embed, a.tok, a.mask, a.M,
+                       d, c.vocab, c.mask_id, (const float*)m->layers[0].g1, w.x, w.xg, m->KCx_d, w.ssq);
+    int n_part = 1;
+
+    const size_t layer_elems = (size_t)2 * H * kv->Cs * Dh;
+    for (int l = 0; l < a.n_layers; ++l) {
+        LayerW& L = m->layers[l];
+        AT* Kc = (AT*)kv->buf + (size_t)l * layer_elems;
+        AT* Vt = Kc + (size_t)H * kv->Cs * Dh;
+
+        // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
+        {
+            GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles,
+                       w.ssq, n_part, w.rows, 1.0f / d, c.eps};
+            EpiQKV<AT> e{d, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, Kc, Vt, kv->Cs};
+            const int F = pick_F(G_QKV, L.qkv.n_tiles, MT);
+            ProbeScope ps(m, DLLM_K_QKV, s);
+            if ((rc = launch_gemm<WT, G_QKV>(F, MT, g, e, ceil_div(L.qkv.n_tiles, F), gy, s))) return rc;
+        }
+        // attention over [0, T) (+ split merge)
+        {
+            AttnArgs at{};
+            at.q = w.q; at.K = Kc; at.Vt = Vt; at.Cs = kv->Cs; at.H = H; at.T = a.T; at.lim = a.lim; at.M = a.M;
+            at.scale = 1.0f / sqrtf((float)Dh); at.o = w.of; at.KCx = m->KCx_d;
+            at.opart = w.opart; at.mlpart = w.mlpart; at.rows_ld = w.wrows;
+            ProbeScope ps(m, DLLM_K_ATTN, s);
+            if (XF32) {
+                at.nsplit = 1; at.bps = 1 << 20;
+                if (Dh == 32) hipLaunchKernelGGL((attn_f32_kernel<32>), dim3(Mc, H), dim3(64), 0, s, at);
+                else if (Dh == 64) hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(Mc, H), dim3(64), 0, s, at);
+                else hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(Mc, H), dim3(64), 0, s, at);
+            } else {
+                const int QT = (a.M <= 64) ? MT : 4;
+                const int nqb = ceil_div(Mc, 16 * QT);
+                const int nblk = ceil_div(a.T, 32);
+                int nsplit = 1;
+                if (a.M <= 64) {
+                    nsplit = std::max(1, std::min(MAX_SPLIT, ceil_div(512, H * nqb)));
+                    nsplit = std::min(nsplit, std::max(1, nblk / 2));
+                }
+                at.bps = ceil_div(nblk, nsplit);
+                at.nsplit = ceil_div(nblk, at.bps);
+                dim3 grid(at.nsplit, H, nqb);
+#define ATTN(DH_, QT_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, QT_>), grid, dim3(64), 0, s, at)
+                if (Dh == 128) {
+                    if (QT == 1) ATTN(128, 1); else if (QT == 2) ATTN(128, 2); else ATTN(128, 4);
+                } else {
+                    if (QT == 1) ATTN(64, 1); else if (QT == 2) ATTN(64, 2); else ATTN(64, 4);
+                }
+#undef ATTN
+                if (at.nsplit > 1) {
+                    const int total = Mc * H * Dh;
+                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(total, 256)), dim3(256), 0, s, at,
+                                       Mc, Dh);
+                }
+            }
+        }
+        // O projection + residual (+ norm-2 operand and partial sums of squares)
+        {
+            GemmArgs g{L.o.w, L.o.scale, w.of, L.o.KCw, L.o.KCw * WTraits<WT>::XPER, L.o.n_tiles,
+                       nullptr, 0, 0, 0.f, 0.f};
+            EpiResidual<XF32> e{w.x, d, a.M, L.g2, w.xg, m->KCx_d, w.ssq, w.rows};
+            ProbeScope ps(m, DLLM_K_OPROJ, s);
+            if ((rc = launch_gemm<WT, G_RES>(1, MT, g, e, L.o.n_tiles, gy, s))) return rc;
+            n_part = L.o.n_tiles;
+        }
+        // RMSNorm + gate/up + SwiGLU
+        {
+            GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles,
+                       w.ssq, n_part, w.rows, 1.0f / d, c.eps};
+            EpiSwiGLU<XF32> e{w.af, m->KCx_f};
+            const int F = pick_F(G_GU, L.gu.n_tiles, MT);
+            ProbeScope ps(m, DLLM_K_GATEUP, s);
+            if ((rc = launch_gemm<WT, G_GU>(F, MT, g, e, ceil_div(L.gu.n_tiles, F), gy, s))) return rc;
+        }
+        // down projection + residual (+ next norm operand)
+        {
+            const float* gnext = (l + 1 < c.n_layers) ? m->layers[l + 1].g1 : m->gf;
+            GemmArgs g{L.down.w, L.down.scale, w.af, L.down.KCw, L.down.KCw * WTraits<WT>::XPER, L.down.n_tiles,
+                       nullptr, 0, 0, 0.f, 0.f};
+            EpiResidual<XF32> e{w.x, d, a.M, gnext, w.xg, m->KCx_d, w.ssq, w.rows};
+            ProbeScope ps(m, DLLM_K_DOWN, s);
+            if ((rc = launch_gemm<WT, G_RES>(1, MT, g, e, L.down.n_tiles, gy, s))) return rc;
+            n_part = L.down.n_tiles;
+        }
+    }
+    if (a.xout) HIP_TRY(hipMemcpyAsync(a.xout, w.x, (size_t)a.M * d * 4, hipMemcpyDeviceToDevice, s));
+    if (a.lm) {
+        if (Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
+        GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles,
+                   w.ssq, n_part, w.rows, 1.0f / d, c.eps};
+        const int F = pick_F(G_LM, m->lm.n_tiles, MT);
+        const int gx = ceil_div(m->lm.n_tiles, F);
+        EpiLM e{c.vocab, c.mask_id, a.M, w.lm, w.wrows, a.logits};
+        {
+            ProbeScope ps(m, DLLM_K_LMHEAD, s);
+            if ((rc = launch_gemm<WT, G_LM>(F, MT, g, e, gx, gy, s))) return rc;
+        }
+        hipLaunchKernelGGL(lm_combine_kernel, dim3(a.M), dim3(64), 0, s, (const LmPartial*)w.lm, gx, w.wrows,
+                           a.out_id, a.out_conf);
+    }
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
+int forward(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
+    if (m->wt == WT_F32) return forward_t<WT_F32, float>(m, kv, a, s);
+    if (m->wt == WT_BF16) return forward_t<WT_BF16, uint16_t>(m, kv, a, s);
+    return forward_t<WT_I8, uint16_t>(m, kv, a, s);
+}
+
+int check_model_kv(const dllm_model* m, const dllm_kv* kv) {
+    if (!m) return fail(DLLM_E_INVAL, "model is NULL");
+    if (!kv) return fail(DLLM_E_INVAL, "kv is NULL");
+    if (kv->model != m) return fail(DLLM_E_INVAL, "kv cache belongs to another model");
+    return DLLM_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+
+extern "C" {
+
+const char* dllm_last_error(void) { return g_last_error.c_str(); }
+
+const char* dllm_version(void) { return "dllm-gfx950 0.1"; }
+
+int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream stream, dllm_model** out) {
+    if (!out) return fail(DLLM_E_INVAL, "out is NULL");
+    *out = nullptr;
+    int rc = validate_config(cfg);
+    if (rc) return rc;
+    if (!w || !w->embed || !w->lm_head || !w->final_norm || !w->layers)
+        return fail(DLLM_E_INVAL, "weights: NULL pointer");
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        const dllm_layer_weights& L = w->layers[l];
+        if (!L.wq || !L.wk || !L.wv || !L.wo || !L.wg || !L.wu || !L.wd || !L.attn_norm || !L.ffn_norm)
+            return fail(DLLM_E_INVAL, "weights: NULL pointer in layer " + std::to_string(l));
+    }
+    hipStream_t s = (hipStream_t)stream;
+    dllm_model* m = new dllm_model();
+    m->cfg = *cfg;
+    const dllm_config& c = m->cfg;
+    m->wt = c.dtype == DLLM_F32 ? WT_F32 : (c.dtype == DLLM_BF16 ? WT_BF16 : WT_I8);
+    m->xf32 = c.dtype == DLLM_F32;
+    m->act_size = m->xf32 ? 4 : 2;
+    const int xcols = m->xf32 ? 16 : 32;
+    const int xper = m->wt == WT_I8 ? 2 : 1;
+    const int d = c.d_model, F = c.d_ff;
+
+    m->layers.resize(c.n_layers);
+    size_t wbytes = 0, srows = 0;
+    for (auto& L : m->layers) {
+        plan_packed(L.qkv, m->wt, 3 * d, d);
+        plan_packed(L.o, m->wt, d, d);
+        plan_packed(L.gu, m->wt, 2 * F, d);
+        plan_packed(L.down, m->wt, d, F);
+        for (PackedW* p : {&L.qkv, &L.o, &L.gu, &L.down}) { wbytes += p->bytes; srows += p->n_tiles * 16; }
+    }
+    plan_packed(m->lm, m->wt, c.vocab, d);
+    wbytes += m->lm.bytes;
+    srows += m->lm.n_tiles * 16;
+    m->KCx_d = m->layers[0].qkv.KCw * xper;
+    m->KCx_f = m->layers[0].down.KCw * xper;
+    (void)xcols;
+    m->n_part_max = std::max(1, m->layers[0].o.n_tiles);
+    m->n_lm_wg = ceil_div(m->lm.n_tiles, std::min(pick_F(G_LM, m->lm.n_tiles, 1), pick_F(G_LM, m->lm.n_tiles, 4)));
+
+    auto cleanup = [&](int code) {
+        dllm_model_destroy(m);
+        return code;
+    };
+    if ((rc = alloc_zero(&m->wpool, wbytes))) return cleanup(rc);
+    if (m->wt == WT_I8 && (rc = alloc_zero((void**)&m->spool, srows * 4))) return cleanup(rc);
+    if ((rc = alloc_zero((void**)&m->gpool, (size_t)(2 * c.n_layers + 1) * d * 4))) return cleanup(rc);
+    const size_t esize = m->xf32 ? 4 : 2;
+    if ((rc = alloc_zero(&m->embed, (size_t)c.vocab * d * esize))) return cleanup(rc);
+    const int half = c.head_dim / 2;
+    if ((rc = alloc_zero((void**)&m->rope, (size_t)c.max_pos * half * sizeof(float2)))) return cleanup(rc);
+
+    // carve
+    char* wp = (char*)m->wpool;
+    float* sp = m->spool;
+    auto carve = [&](PackedW& p) {
+        p.w = wp;
+        wp += p.bytes;
+        if (sp) { p.scale = sp; sp += p.n_tiles * 16; }
+    };
+    for (auto& L : m->layers) { carve(L.qkv); carve(L.o); carve(L.gu); carve(L.down); }
+    carve(m->lm);
+    for (int l = 0; l < c.n_layers; ++l) {
+        m->layers[l].g1 = m->gpool + (size_t)(2 * l) * d;
+        m->layers[l].g2 = m->gpool + (size_t)(2 * l + 1) * d;
+    }
+    m->gf = m->gpool + (size_t)(2 * c.n_layers) * d;
+
+    // pack
+    const bool src_f32 = (c.dtype == DLLM_F32);
+    auto pack = [&](PackedW& p, int kind, const void* a0, const void* a1, const void* a2) -> int {
+        PackSrc src{{a0, a1, a2}, kind, p.N, p.K, d, c.head_dim};
+        return src_f32 ? pack_one<float>(m, p, src, s) : pack_one<uint16_t>(m, p, src, s);
+    };
+    for (int l = 0; l < c.n_layers; ++l) {
+        const dllm_layer_weights& S = w->layers[l];
+        LayerW& L = m->layers[l];
+        if ((rc = pack(L.qkv, MAP_QKV, S.wq, S.wk, S.wv))) return cleanup(rc);
+        if ((rc = pack(L.o, MAP_IDENT, S.wo, nullptr, nullptr))) return cleanup(rc);
+        if ((rc = pack(L.gu, MAP_GATEUP, S.wg, S.wu, nullptr))) return cleanup(rc);
+        if ((rc = pack(L.down, MAP_IDENT, S.wd, nullptr, nullptr))) return cleanup(rc);
+        if (hipMemcpyAsync(L.g1, S.attn_norm, d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(L.g2, S.ffn_norm, d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+            return cleanup(fail(DLLM_E_HIP, "copying norm gains failed"));
+    }
+    if ((rc = pack(m->lm, MAP_IDENT, w->lm_head, nullptr, nullptr))) return cleanup(rc);
+    if (hipMemcpyAsync(m->gf, w->final_norm, d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(m->embed, w->embed, (size_t)c.vocab * d * esize, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return cleanup(fail(DLLM_E_HIP, "copying embedding / final norm failed"));
+    {
+        const size_t n = (size_t)c.max_pos * half;
+        hipLaunchKernelGGL(rope_table_kernel, dim3(ceil_div((long)n, 256)), dim3(256), 0, s, m->rope, c.max_pos, half,
+                           (double)c.rope_base);
+    }
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+        return cleanup(fail(DLLM_E_HIP, "weight prepacking failed"));
+    if ((rc = ensure_ws(m, c.max_window))) return cleanup(rc);
+    *out = m;
+    return DLLM_OK;
+}
+
+int dllm_model_destroy(dllm_model* m) {
+    if (!m) return DLLM_OK;
+    free_ws(m->ws);
+    void* ptrs[] = {m->wpool, m->spool, m->gpool, m->embed, m->rope};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    for (auto e : m->ev_b) (void)hipEventDestroy(e);
+    for (auto e : m->ev_e) (void)hipEventDestroy(e);
+    delete m;
+    return DLLM_OK;
+}
+
+static int cs_of(int capacity) { return (int)round_up(capacity, 32); }
+
+int dllm_kv_bytes(const dllm_model* m, int32_t capacity, size_t* bytes) {
+    if (!m || !bytes) return fail(DLLM_E_INVAL, "NULL argument");
+    if (capacity < 1 || capacity > m->cfg.max_pos)
+        return fail(DLLM_E_CAPACITY, "capacity must be in [1, max_pos]");
+    const dllm_config& c = m->cfg;
+    *bytes = (size_t)c.n_layers * 2 * c.n_heads * cs_of(capacity) * c.head_dim * m->act_size;
+    return DLLM_OK;
+}
+
+int dllm_kv_create(const dllm_model* m, void* d_buf, size_t bytes, int32_t capacity, dllm_kv** out) {
+    if (!out) return fail(DLLM_E_INVAL, "out is NULL");
+    *out = nullptr;
+    size_t need = 0;
+    int rc = dllm_kv_bytes(m, capacity, &need);
+    if (rc) return rc;
+    if (!d_buf) return fail(DLLM_E_INVAL, "buffer is NULL");
+    if (bytes < need) return fail(DLLM_E_CAPACITY, "buffer smaller than dllm_kv_bytes()");
+    if (((uintptr_t)d_buf & 15) != 0) return fail(DLLM_E_INVAL, "buffer must be 16-byte aligned");
+    *out = new dllm_kv{m, d_buf, bytes, capacity, cs_of(capacity), 0, 0};
+    return DLLM_OK;
+}
+
+int dllm_kv_destroy(dllm_kv* kv) {
+    delete kv;
+    return DLLM_OK;
+}
+
+int dllm_kv_prefix_len(const dllm_kv* kv, int32_t* prefix_len, int32_t* prompt_len) {
+    if (!kv) return fail(DLLM_E_INVAL, "kv is NULL");
+    if (prefix_len) *prefix_len = kv->prefix_len;
+    if (prompt_len) *prompt_len = kv->prompt_len;
+    return DLLM_OK;
+}
+
+int dllm_kv_set_prefix_len(dllm_kv* kv, int32_t prefix_len) {
+    if (!kv) return fail(DLLM_E_INVAL, "kv is NULL");
+    if (prefix_len < kv->prompt_len || prefix_len > kv->capacity)
+        return fail(DLLM_E_INVAL, "prefix_len must be in [prompt_len, capacity]");
+    kv->prefix_len = prefix_len;
+    return DLLM_OK;
+}
+
+int dllm_prefill(dllm_model* m, dllm_kv* kv, const int32_t* d_ids, int32_t n, dllm_stream stream) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (!d_ids) return fail(DLLM_E_INVAL, "ids is NULL");
+    if (n < 1) return fail(DLLM_E_INVAL, "n must be >= 1");
+    if (kv->prefix_len != 0) return fail(DLLM_E_INVAL, "prefill needs an empty cache");
+    if (n > kv->capacity) return fail(DLLM_E_CAPACITY, "prompt longer than the cache capacity");
+    FwdArgs a{};
+    a.M = n; a.tok = d_ids; a.mask = nullptr; a.pos_base = 0; a.pos = nullptr; a.T = n; a.lim = nullptr;
+    a.n_layers = m->cfg.n_layers; a.lm = false;
+    if ((rc = forward(m, kv, a, (hipStream_t)stream))) return rc;
+    kv->prefix_len = n;
+    kv->prompt_len = n;
+    return DLLM_OK;
+}
+
+static int window_checks(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, int32_t W) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (!d_tok) return fail(DLLM_E_INVAL, "tokens pointer is NULL");
+    if (W < 1 || W > m->cfg.max_window) return fail(DLLM_E_INVAL, "W must be in [1, max_window]");
+    if (kv->prefix_len + W > kv->capacity) return fail(DLLM_E_CAPACITY, "prefix_len + W exceeds the cache capacity");
+    return DLLM_OK;
+}
+
+int dllm_denoise_step(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
+                      int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
+    int rc = window_checks(m, kv, d_tok, W);
+    if (rc) return rc;
+    if (!d_out_id || !d_out_conf) return fail(DLLM_E_INVAL, "output pointer is NULL");
+    FwdArgs a{};
+    a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + W;
+    a.n_layers = m->cfg.n_layers; a.lm = true; a.out_id = d_out_id; a.out_conf = d_out_conf;
+    return forward(m, kv, a, (hipStream_t)stream);
+}
+
+int dllm_debug_logits(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
+                      float* d_logits, int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
+    int rc = window_checks(m, kv, d_tok, W);
+    if (rc) return rc;
+    if (!d_logits) return fail(DLLM_E_INVAL, "logits pointer is NULL");
+    FwdArgs a{};
+    a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + W;
+    a.n_layers = m->cfg.n_layers; a.lm = true; a.logits = d_logits; a.out_id = d_out_id; a.out_conf = d_out_conf;
+    return forward(m, kv, a, (hipStream_t)stream);
+}
+
+int dllm_debug_hidden(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
+                      int32_t n_layers, float* d_x, dllm_stream stream) {
+    int rc = window_checks(m, kv, d_tok, W);
+    if (rc) return rc;
+    if (!d_x) return fail(DLLM_E_INVAL, "output pointer is NULL");
+    if (n_layers < 0 || n_layers > m->cfg.n_layers) return fail(DLLM_E_INVAL, "n_layers out of range");
+    FwdArgs a{};
+    a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + W;
+    a.n_layers = n_layers; a.lm = false; a.xout = d_x;
+    return forward(m, kv, a, (hipStream_t)stream);
+}
+
+int dllm_commit(const float* d_conf, const int32_t* d_id, int32_t* d_tok, uint8_t* d_mask, int32_t seg_begin,
+                int32_t seg_len, int32_t k, int32_t* d_committed_pos, int32_t* d_n_committed, dllm_stream stream) {
+    if (!d_conf || !d_id || !d_tok || !d_mask) return fail(DLLM_E_INVAL, "NULL argument");
+    if (k < 0) return fail(DLLM_E_INVAL, "k must be >= 0");
+    if (seg_begin < 0 || seg_len < 0 || seg_len > 1024) return fail(DLLM_E_INVAL, "segment out of range");
+    hipLaunchKernelGGL(commit_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, d_conf, d_id, d_tok, d_mask,
+                       seg_begin, seg_len, k, d_committed_pos, d_n_committed);
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
+int dllm_append_prefix_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_block_tok, int32_t n, dllm_stream stream) {
+    int rc = window_checks(m, kv, d_block_tok, n);
+    if (rc) return rc;
+    FwdArgs a{};
+    a.M = n; a.tok = d_block_tok; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + n;
+    a.n_layers = m->cfg.n_layers; a.lm = false;
+    if ((rc = forward(m, kv, a, (hipStream_t)stream))) return rc;
+    kv->prefix_len += n;
+    return DLLM_OK;
+}
+
+int dllm_refresh_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_pos, const int32_t* d_new_id, int32_t n,
+                    int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (!d_pos || !d_new_id) return fail(DLLM_E_INVAL, "NULL argument");
+    if (n < 1 || n > m->cfg.max_window) return fail(DLLM_E_INVAL, "n must be in [1, max_window]");
+    if ((d_out_id == nullptr) != (d_out_conf == nullptr))
+        return fail(DLLM_E_INVAL, "out_id and out_conf must both be set or both be NULL");
+    hipStream_t s = (hipStream_t)stream;
+    std::vector<int32_t> pos(n);
+    HIP_TRY(hipMemcpyAsync(pos.data(), d_pos, (size_t)n * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    std::vector<int32_t> sorted(pos);
+    std::sort(sorted.begin(), sorted.end());
+    for (int i = 0; i < n; ++i) {
+        if (sorted[i] < 0 || sorted[i] >= kv->prefix_len)
+            return fail(DLLM_E_INVAL, "refresh position outside [0, prefix_len)");
+        if (i > 0 && sorted[i] == sorted[i - 1]) return fail(DLLM_E_INVAL, "refresh positions must be distinct");
+    }
+    int T = 0;
+    for (int p : pos) {
+        const int e = (p < kv->prompt_len) ? kv->prompt_len
+                                           : kv->prompt_len + m->cfg.block * (1 + (p - kv->prompt_len) / m->cfg.block);
+        T = std::max(T, std::min(e, kv->prefix_len));
+    }
+    if ((rc = ensure_ws(m, n))) return rc;
+    HIP_TRY(hipMemcpyAsync(m->ws.pos, d_pos, (size_t)n * 4, hipMemcpyDeviceToDevice, s));
+    hipLaunchKernelGGL(refresh_limits_kernel, dim3(ceil_div(n, 64)), dim3(64), 0, s, d_pos, n, kv->prompt_len,
+                       m->cfg.block, kv->prefix_len, m->ws.lim);
+    FwdArgs a{};
+    a.M = n; a.tok = d_new_id; a.pos = m->ws.pos; a.T = T; a.lim = m->ws.lim;
+    a.n_layers = m->cfg.n_layers; a.lm = d_out_id != nullptr; a.out_id = d_out_id; a.out_conf = d_out_conf;
+    return forward(m, kv, a, s);
+}
+
+int dllm_probe_enable(dllm_model* m, int32_t kernel_class, int32_t max_records) {
+    if (!m) return fail(DLLM_E_INVAL, "model is NULL");
+    if (kernel_class < 0) { m->probe_class = -1; return DLLM_OK; }
+    if (kernel_class > DLLM_K_LMHEAD || max_records < 1) return fail(DLLM_E_INVAL, "bad probe arguments");
+    while ((int)m->ev_b.size() < max_records) {
+        hipEvent_t b, e;
+        HIP_TRY(hipEventCreate(&b));
+        HIP_TRY(hipEventCreate(&e));
+        m->ev_b.push_back(b);
+        m->ev_e.push_back(e);
+    }
+    m->probe_class = kernel_class;
+    m->probe_max = max_records;
+    m->probe_n = 0;
+    return DLLM_OK;
+}
+
+int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms) {
+    if (!m || !n_records || !mean_ms) return fail(DLLM_E_INVAL, "NULL argument");
+    double tot = 0;
+    for (int i = 0; i < m->probe_n; ++i) {
+        HIP_TRY(hipEventSynchronize(m->ev_e[i]));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, m->ev_b[i], m->ev_e[i]));
+        tot += ms;
+    }
+    *n_records = m->probe_n;
+    *mean_ms = m->probe_n ? tot / m->probe_n : 0.0;
+    m->probe_n = 0;
+    return DLLM_OK;
+}
+
+int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes) {
+    if (!m || !bytes) return fail(DLLM_E_INVAL, "NULL argument");
+    const dllm_config& c = m->cfg;
+    const double wsz = m->wt == WT_F32 ? 4.0 : (m->wt == WT_BF16 ? 2.0 : 1.0);
+    const double asz = (double)m->act_size;
+    const double d = c.d_model, F = c.d_ff, V = c.vocab;
+    const double scale_b = (m->wt == WT_I8) ? 4.0 : 0.0;   // per weight row
+    double b = 0;
+    switch (kernel_class) {
+        case DLLM_K_QKV: b = 3 * d * d * wsz + 3 * d * scale_b + W * d * asz + 2.0 * W * d * asz + W * d * asz; break;
+        case DLLM_K_ATTN: b = 2.0 * (P + W) * d * asz + 2.0 * W * d * asz; break;
+        case DLLM_K_OPROJ: b = d * d * wsz + d * scale_b + W * d * asz + 2.0 * W * d * 4 + W * d * asz; break;
+        case DLLM_K_GATEUP: b = 2 * F * d * wsz + 2 * F * scale_b + W * d * asz + W * F * asz; break;
+        case DLLM_K_DOWN: b = d * F * wsz + d * scale_b + W * F * asz + 2.0 * W * d * 4 + W * d * asz; break;
+        case DLLM_K_LMHEAD: b = V * d * wsz + V * scale_b + W * d * asz; break;
+        default: return fail(DLLM_E_INVAL, "unknown kernel class");
+    }
+    *bytes = b;
+    return DLLM_OK;
+}
+
+}  // extern "C"

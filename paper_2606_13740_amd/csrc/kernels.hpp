@@ -1,0 +1,245 @@
+// Small kernels around the GEMMs: embedding gather, LM-head merge, commit,
+// weight prepacking / int8 quantisation and the RoPE table.
+#pragma once
+
+#include "common.hpp"
+#include "gemm.hpp"
+
+namespace dllm {
+
+// ---------------------------------------------------------------------------
+// Embedding gather: x[m] = E[id_m] (the MASK id where the mask flag is set), the
+// first RMSNorm's A operand x * g, and sum(x^2) as the single norm partial.
+// ---------------------------------------------------------------------------
+template <typename ET, bool XF32>
+__global__ void __launch_bounds__(256)
+embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int V, int mask_id,
+             const float* g, float* x, void* xg, int KCx, float* ssq) {
+    __shared__ float red[4];
+    const int m = blockIdx.x;
+    float sq = 0.f;
+    if (m < M) {
+        int id = (mask != nullptr && mask[m]) ? mask_id : tok[m];
+        if (id < 0 || id >= V) id = mask_id;
+        const ET* row = E + (size_t)id * d;
+        for (int n = threadIdx.x; n < d; n += blockDim.x) {
+            const float v = to_f32<ET>(row[n]);
+            x[(size_t)m * d + n] = v;
+            xfrag_store<XF32>(xg, m, n, KCx, v * g[n]);
+            sq += v * v;
+        }
+    } else {
+        for (int n = threadIdx.x; n < d; n += blockDim.x) {
+            x[(size_t)m * d + n] = 0.f;
+            xfrag_store<XF32>(xg, m, n, KCx, 0.f);
+        }
+    }
+    sq = warp_sum(sq);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
+    __syncthreads();
+    if (threadIdx.x == 0) ssq[m] = red[0] + red[1] + red[2] + red[3];
+}
+
+// ---------------------------------------------------------------------------
+// LM-head merge across vocabulary tiles -> id, confidence = 1 / sum exp(l - max)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ LmPartial lm_merge(LmPartial a, LmPartial b) {
+    if (b.arg < 0) return a;
+    if (a.arg < 0) return b;
+    LmPartial o;
+    o.mx = fmaxf(a.mx, b.mx);
+    if (a.mx > b.mx) o.arg = a.arg;
+    else if (b.mx > a.mx) o.arg = b.arg;
+    else o.arg = min(a.arg, b.arg);
+    o.s = a.s * expf(a.mx - o.mx) + b.s * expf(b.mx - o.mx);
+    o.pad = 0.f;
+    return o;
+}
+
+__global__ void __launch_bounds__(64)
+lm_combine_kernel(const LmPartial* part, int n_wg, int part_ld, int* out_id, float* out_conf) {
+    const int m = blockIdx.x;
+    const int lane = threadIdx.x;
+    LmPartial acc{-INFINITY, -1, 0.f, 0.f};
+    for (int w = lane; w < n_wg; w += 64) acc = lm_merge(acc, part[(size_t)w * part_ld + m]);
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        LmPartial o;
+        o.mx = __shfl_xor(acc.mx, off);
+        o.arg = __shfl_xor(acc.arg, off);
+        o.s = __shfl_xor(acc.s, off);
+        o.pad = 0.f;
+        // combine in lane order so every lane computes the same merge
+        acc = (lane & off) ? lm_merge(o, acc) : lm_merge(acc, o);
+    }
+    if (lane == 0) {
+        if (out_id) out_id[m] = acc.arg;
+        if (out_conf) out_conf[m] = 1.0f / acc.s;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Commit: top-k masked positions of a segment by confidence (ties -> lower
+// position).  Every thread ranks its positions against the whole segment.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+commit_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, int seg_begin, int seg_len,
+              int k, int* committed, int* n_committed) {
+    __shared__ float c_s[1024];
+    __shared__ uint8_t m_s[1024];
+    __shared__ int cnt;
+    if (threadIdx.x == 0) cnt = 0;
+    __syncthreads();
+    int local = 0;
+    for (int i = threadIdx.x; i < seg_len; i += blockDim.x) {
+        const uint8_t mk = mask[seg_begin + i];
+        m_s[i] = mk;
+        c_s[i] = conf[seg_begin + i];
+        local += mk ? 1 : 0;
+    }
+    atomicAdd(&cnt, local);
+    __syncthreads();
+    for (int i = threadIdx.x; i < seg_len; i += blockDim.x) {
+        if (!m_s[i]) continue;
+        const float ci = c_s[i];
+        int rank = 0;
+        for (int j = 0; j < seg_len; ++j)
+            if (m_s[j] && (c_s[j] > ci || (c_s[j] == ci && j < i))) ++rank;
+        if (rank < k) {
+            const int p = seg_begin + i;
+            tok[p] = id[p];
+            mask[p] = 0;
+            if (committed) committed[rank] = p;
+        }
+    }
+    if (threadIdx.x == 0 && n_committed) *n_committed = min(k, cnt);
+}
+
+// ---------------------------------------------------------------------------
+// Weight prepacking into MFMA chunks.  Packed row r takes source row
+// rowmap(r) of one of up to three source matrices (or zeros for padding).
+// ---------------------------------------------------------------------------
+enum RowMap : int { MAP_IDENT = 0, MAP_QKV = 1, MAP_GATEUP = 2 };
+
+struct PackSrc {
+    const void* src[3];
+    int kind;
+    int N;        // real packed rows
+    int K;        // real columns
+    int d, Dh;    // for MAP_QKV
+};
+
+__device__ __forceinline__ const void* src_row(const PackSrc& p, int r, int& row) {
+    if (r >= p.N) return nullptr;
+    if (p.kind == MAP_IDENT) { row = r; return p.src[0]; }
+    if (p.kind == MAP_GATEUP) { row = r >> 1; return p.src[r & 1]; }
+    const int seg = r / p.d, rr = r - seg * p.d;
+    if (seg == 2) { row = rr; return p.src[2]; }
+    const int h = rr / p.Dh, w = rr - h * p.Dh;
+    row = h * p.Dh + (w >> 1) + (w & 1) * (p.Dh >> 1);   // adjacent packed rows = RoPE pair
+    return p.src[seg];
+}
+
+// One thread per 16-byte lane slot.  ST: source element type (float / uint16_t bf16).
+template <int WT, typename ST>
+__global__ void __launch_bounds__(256)
+pack_kernel(PackSrc p, int n_tiles, int KCw, u32x4_t* out, const float* scale) {
+    const size_t u = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t total = (size_t)n_tiles * KCw * 64;
+    if (u >= total) return;
+    const int lane = (int)(u & 63);
+    const size_t ch = u >> 6;
+    const int kc = (int)(ch % KCw);
+    const int nt = (int)(ch / KCw);
+    const int r = nt * 16 + (lane & 15), g = lane >> 4;
+    int row = 0;
+    const ST* src = (const ST*)src_row(p, r, row);
+    u32x4_t v = {0u, 0u, 0u, 0u};
+    if (src != nullptr) {
+        const ST* s = src + (size_t)row * p.K;
+        if constexpr (WT == WT_BF16) {
+            uint16_t e[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int k = kc * 32 + 8 * g + i;
+                e[i] = (k < p.K) ? f32_to_bf16(to_f32<ST>(s[k])) : (uint16_t)0;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = (uint32_t)e[2 * i] | ((uint32_t)e[2 * i + 1] << 16);
+        } else if constexpr (WT == WT_F32) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int k = kc * 16 + 4 * q + g;
+                v[q] = __float_as_uint((k < p.K) ? to_f32<ST>(s[k]) : 0.f);
+            }
+        } else {
+            const float sc = scale[r];
+            uint32_t b[16];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int k = kc * 64 + 32 * hh + 8 * g + e;
+                    int qv = 0;
+                    if (k < p.K && sc > 0.f) {
+                        qv = (int)rintf(__fdiv_rn(to_f32<ST>(s[k]), sc));
+                        qv = max(-127, min(127, qv));
+                    }
+                    b[8 * hh + e] = (uint32_t)(qv & 0xFF);
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                v[i] = b[4 * i] | (b[4 * i + 1] << 8) | (b[4 * i + 2] << 16) | (b[4 * i + 3] << 24);
+        }
+    }
+    out[u] = v;
+}
+
+// Per packed row: s = max |w| / 127 (fp32, correctly rounded division).
+template <typename ST>
+__global__ void __launch_bounds__(256) row_scale_kernel(PackSrc p, int n_rows_padded, float* scale) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    int row = 0;
+    const ST* src = (const ST*)src_row(p, r, row);
+    float mx = 0.f;
+    if (src != nullptr) {
+        const ST* s = src + (size_t)row * p.K;
+        for (int k = threadIdx.x; k < p.K; k += blockDim.x) mx = fmaxf(mx, fabsf(to_f32<ST>(s[k])));
+    }
+    mx = warp_max(mx);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0 && r < n_rows_padded)
+        scale[r] = __fdiv_rn(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])), 127.0f);
+}
+
+// (cos, sin) of pos * base^(-2j/Dh), evaluated in double.
+__global__ void __launch_bounds__(256) rope_table_kernel(float2* t, int max_pos, int half, double base) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (size_t)max_pos * half) return;
+    const int j = (int)(i % half);
+    const int p = (int)(i / half);
+    const double inv = pow(base, -2.0 * j / (2.0 * half));
+    const double th = (double)p * inv;
+    t[i] = make_float2((float)cos(th), (float)sin(th));
+}
+
+// Copy with element conversion (embedding / gains into the library's own copy).
+template <typename ST, typename DT>
+__global__ void __launch_bounds__(256) convert_kernel(const ST* s, DT* d, size_t n) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) d[i] = from_f32<DT>(to_f32<ST>(s[i]));
+}
+
+// Per-row key limit of refreshed rows: end of the row's block, capped at the prefix.
+__global__ void refresh_limits_kernel(const int* pos, int n, int prompt_len, int block, int prefix_len,
+                                      int* lim) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int p = pos[i];
+    int e = (p < prompt_len) ? prompt_len : prompt_len + block * (1 + (p - prompt_len) / block);
+    lim[i] = min(e, prefix_len);
+}
+
+}  // namespace dllm
