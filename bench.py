@@ -1,0 +1,194 @@
+"""Benchmark: denoising steps/s of block-wise diffusion-LLM inference on one MI355X.
+
+Workload (default): one LLaDA-8B-shaped denoising step in bf16 with random
+N(0, 0.02) weights: 32 layers, d 4096, 32 heads x 128, SwiGLU 12288, vocab
+126464; a prefix KV cache of 512 tokens prefilled from random prompt ids; a
+32-token block with 24 MASK and 8 committed random ids; each step is
+dllm_denoise_step + dllm_commit(k=1).  Inputs are synthetic and resident in HBM
+before the timed region.
+
+Prints ONE JSON line with the metric, a roofline record for the dominant kernel
+(gate/up projection: the largest share of a step's time) and the CPU oracle's
+throughput on a bounded sample of the same step.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+WORKLOADS = {
+    # name: (shape, dtype, prefix, window, masked rows, commits per segment, segments)
+    "llada8b_bf16_p512_w32": dict(shape="llada8b", dtype="bf16", prefix=512, W=32,
+                                  masked=list(range(8, 32)), segs=[(0, 32, 1)]),
+    "llada8b_bf16_p1024_w64_spec": dict(shape="llada8b", dtype="bf16", prefix=1024, W=64,
+                                        masked=list(range(24, 64)), segs=[(0, 32, 4), (32, 32, 4)]),
+    "llada8b_w8_p4096_w64_spec": dict(shape="llada8b", dtype="w8", prefix=4096, W=64,
+                                      masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)]),
+}
+DEFAULT = "llada8b_bf16_p512_w32"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob):
+    """Oracle (float64 NumPy) on a bounded sample: one layer of the step plus the
+    full LM head, scaled to the whole 32-layer step."""
+    import oracle
+
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    sh1 = shape.with_layers(1)
+    om = oracle.OracleModel(sh1, dict(glob, layers=None), int8=(dtype == "w8"), cache_layers=True,
+                            layer_source=lambda l: synth.layer_weights(shape, l, "bf16"))
+    kv = oracle.OracleKV(sh1, wl["prefix"] + wl["W"])
+    oracle.prefill(om, kv, prompt)        # setup, not timed
+    P, W = wl["prefix"], wl["W"]
+    ids = oracle.input_ids(shape, tok, mask)
+    t0 = time.perf_counter()
+    x, _ = oracle.forward_rows(om, kv, ids, P + np.arange(W), np.full(W, P + W), lm_head=False)
+    t1 = time.perf_counter()
+    logits = om.lm_logits(oracle.rmsnorm(x, om.final_norm, shape.eps))
+    oracle.confidence(logits)
+    t2 = time.perf_counter()
+    step_s = shape.n_layers * (t1 - t0) + (t2 - t1)
+    return {"value": 1.0 / step_s, "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"1 of {shape.n_layers} layers of the step ({t1 - t0:.2f} s) + the full LM head "
+                      f"({t2 - t1:.2f} s), layer time scaled x{shape.n_layers}; float64 NumPy"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path has no multi-GPU mode",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_13740_amd as dl
+
+    wl = WORKLOADS[args.workload]
+    shape = synth.PRESETS[wl["shape"]]
+    dtype = wl["dtype"]
+    P, W = wl["prefix"], wl["W"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t0 = time.time()
+    glob = synth.global_weights(shape, "bf16")
+    model = dl.Model(shape, dtype, glob, lambda l: synth.layer_weights(shape, l, "bf16"),
+                     max_window=64, max_pos=P + W + 64)
+    log(f"model created in {time.time() - t0:.1f} s")
+    kv = dl.KVCache(model, P + W)
+    prompt = synth.prompt_ids(shape, P)
+    dl.dllm_prefill(model.handle, kv.handle, torch.from_numpy(prompt).to(dev), P)
+    tok, mask = synth.window(shape, W, wl["masked"])
+    d_tok0 = torch.from_numpy(tok).to(dev)
+    d_mask0 = torch.from_numpy(mask).to(dev)
+    d_tok, d_mask = d_tok0.clone(), d_mask0.clone()
+    ids = torch.empty(W, dtype=torch.int32, device=dev)
+    conf = torch.empty(W, device=dev)
+    cpos = torch.empty(64, dtype=torch.int32, device=dev)
+    ncom = torch.empty(4, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    log(f"prefill {P} done")
+
+    def step():
+        dl.dllm_denoise_step(model.handle, kv.handle, d_tok, d_mask, W, ids, conf)
+        for j, (b, n, k) in enumerate(wl["segs"]):
+            dl.dllm_commit(conf, ids, d_tok, d_mask, b, n, k, cpos[16 * j:], ncom[j:])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    d_tok.copy_(d_tok0)
+    d_mask.copy_(d_mask0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = e0.elapsed_time(e1) / args.steps
+    steps_s = 1000.0 / ms
+    commits = sum(k for _, _, k in wl["segs"])
+    log(f"{ms:.3f} ms/step (GPU events), wall {1000 * wall / args.steps:.3f} ms/step")
+
+    # Per-kernel durations (HIP events around each launch of one kernel class, on the
+    # launch stream), in a separate pass so the probe's events do not perturb the timing.
+    kern = {}
+    step_bytes = 0.0
+    for name, cls in dl.KERNEL_CLASSES.items():
+        nl = 1 if name == "lmhead" else shape.n_layers
+        dl.dllm_probe_enable(model.handle, cls, nl * 4)
+        for _ in range(4):
+            step()
+        n, mean_ms = dl.dllm_probe_read(model.handle)
+        dl.dllm_probe_enable(model.handle, -1, 1)
+        b = dl.dllm_kernel_bytes(model.handle, cls, W, P)
+        kern[name] = {"launches_per_step": nl, "mean_us": mean_ms * 1e3, "alg_bytes": b,
+                      "gbs": b / (mean_ms * 1e-3) / 1e9 if mean_ms > 0 else None}
+        step_bytes += nl * b
+    busy_ms = sum(v["launches_per_step"] * v["mean_us"] / 1e3 for v in kern.values())
+    dom = "gateup"
+    dk = kern[dom]
+    roof = {"bound": "hbm", "achieved": round(dk["gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "gemm gate/up + SwiGLU",
+            "alg_bytes_per_launch": dk["alg_bytes"]}
+
+    out = {
+        "metric": "denoising steps/sec + tokens/sec, LLaDA-8B shape, block 32; % of HBM roofline",
+        "value": round(steps_s, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if dtype == "bf16" else "int8w-bf16a",
+        "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
+        "config": {"workload": args.workload, "layers": shape.n_layers, "d_model": shape.d_model,
+                   "heads": shape.n_heads, "head_dim": shape.head_dim, "d_ff": shape.d_ff, "vocab": shape.vocab,
+                   "prefix": P, "window": W, "masked": len(wl["masked"]), "commits_per_step": commits},
+        "query_tok_s": round(W * steps_s, 1),
+        "committed_tok_s": round(commits * steps_s, 1),
+        "step_hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_alg_gb": round(step_bytes / 1e9, 3),
+        "kernel_busy_ms": round(busy_ms, 4),
+        "kernels": {k: {kk: (round(vv, 2) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in kern.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        out["cpu_baseline"] = cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob)
+        log(f"cpu baseline in {time.time() - t0:.1f} s")
+    kv.close()
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

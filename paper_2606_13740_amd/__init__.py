@@ -281,19 +281,25 @@ class KVCache:
         return (self.capacity + 31) // 32 * 32
 
     def views(self):
-        """(K [L][H][Cs][Dh], V^T [L][H][Dh][Cs]) torch views of the buffer."""
+        """(K [L][H][Cs][Dh], V^T [L][H][Dh][Cs]) as float32 tensors.
+
+        fp32 models: views of the buffer.  bf16 / int8 models: hi + lo of the two
+        bf16 planes (a new tensor, not a view)."""
         import torch
 
         sh = self.model.shape
-        el = torch.float32 if self.model.dtype == "f32" else torch.bfloat16
-        esz = 4 if el == torch.float32 else 2
         Cs = self.row_stride
-        n = sh.n_layers * 2 * sh.n_heads * Cs * sh.head_dim
-        flat = self.buf.view(torch.uint8)[: n * esz].view(el)
-        per = flat.view(sh.n_layers, 2, sh.n_heads, Cs * sh.head_dim)
-        K = per[:, 0].view(sh.n_layers, sh.n_heads, Cs, sh.head_dim)
-        Vt = per[:, 1].view(sh.n_layers, sh.n_heads, sh.head_dim, Cs)
-        return K, Vt
+        plane = sh.n_heads * Cs * sh.head_dim
+        if self.model.dtype == "f32":
+            flat = self.buf.view(torch.uint8)[: sh.n_layers * 2 * plane * 4].view(torch.float32)
+            per = flat.view(sh.n_layers, 2, plane)
+            K, Vt = per[:, 0], per[:, 1]
+        else:
+            flat = self.buf.view(torch.uint8)[: sh.n_layers * 4 * plane * 2].view(torch.bfloat16)
+            per = flat.view(sh.n_layers, 4, plane).float()
+            K, Vt = per[:, 0] + per[:, 1], per[:, 2] + per[:, 3]
+        return (K.reshape(sh.n_layers, sh.n_heads, Cs, sh.head_dim),
+                Vt.reshape(sh.n_layers, sh.n_heads, sh.head_dim, Cs))
 
     @property
     def prefix_len(self) -> int:

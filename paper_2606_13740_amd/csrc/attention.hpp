@@ -5,7 +5,7 @@
 // range is cut into 32-key blocks; each wave streams its share of blocks with
 // an online softmax; splits of the key range are merged by attn_combine.
 //
-// bf16 path on MFMA, computed transposed so that no operand needs a shuffle:
+// MFMA path, computed transposed so that no operand needs a shuffle:
 //   S^T (16 keys x 16 queries) = K_tile (A: 16 keys x 32 dims) * Q^T (B)
 //   O^T (16 dims x 16 queries) += V^T_tile (A: 16 dims x 32 keys) * P^T (B)
 // K rows are loaded in the order key = 8*(r/4) + 4t + r%4 for tile t, so that
@@ -20,8 +20,10 @@ namespace dllm {
 
 struct AttnArgs {
     const void* q;        // [rows][H][Dh]
+    size_t q_plane;       // elements from the hi to the lo plane of q (bf16 path)
     const void* K;        // layer base [H][Cs][Dh]
     const void* Vt;       // layer base [H][Dh][Cs]
+    size_t kv_plane;      // elements from the hi to the lo plane of K and V^T (bf16 path)
     int Cs;               // cache row stride (multiple of 32)
     int H;
     int T;                // keys [0, T) for rows without their own limit
@@ -36,6 +38,9 @@ struct AttnArgs {
     int rows_ld;
 };
 
+// bf16 MFMA path.  Q, K and V are carried as hi + lo bf16 planes and each
+// product takes three MFMAs (hi*hi + hi*lo + lo*hi), so scores and outputs keep
+// ~16 significant bits; the probabilities P are split the same way.
 template <int DH, int QT>
 __global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
     constexpr int NC = DH / 32;     // 32-dim chunks
@@ -51,13 +56,17 @@ __global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
     const uint16_t* Kp = (const uint16_t*)a.K + (size_t)h * a.Cs * DH;
     const uint16_t* Vp = (const uint16_t*)a.Vt + (size_t)h * DH * a.Cs;
 
-    u32x4_t qf[QT][NC];
+    u32x4_t qf[QT][NC][2];
     int lim[QT];
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
         const int row = row0 + 16 * t + r;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) qf[t][c] = ldg16(qp + (size_t)row * ld + h * DH + 32 * c + 8 * g);
+        for (int c = 0; c < NC; ++c) {
+            const uint16_t* src = qp + (size_t)row * ld + h * DH + 32 * c + 8 * g;
+            qf[t][c][0] = ldg16(src);
+            qf[t][c][1] = ldg16(src + a.q_plane);
+        }
         lim[t] = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
     }
 
@@ -78,71 +87,92 @@ __global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
 
     for (int kb = kb0; kb < kb1; ++kb) {
         const int k0 = kb * 32;
-        u32x4_t kf[2][NC];
+        // scores S^T for both 16-key tiles and every query tile
+        f32x4_t sacc[2][QT];
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                kf[t][c] = ldg16(Kp + (size_t)(k0 + krow0 + 4 * t) * DH + 32 * c + 8 * g);
-        u32x4_t vf[ND];
+            for (int u = 0; u < QT; ++u) sacc[t][u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) vf[dt] = ldg16(Vp + (size_t)(16 * dt + r) * a.Cs + k0 + 8 * g);
-        if (k0 + 8 * g + 8 > a.T) {            // tail: zero V beyond T (the rows may be unwritten)
+        for (int c = 0; c < NC; ++c) {
+            u32x4_t kf[2][2];
 #pragma unroll
-            for (int dt = 0; dt < ND; ++dt)
+            for (int t = 0; t < 2; ++t) {
+                const uint16_t* src = Kp + (size_t)(k0 + krow0 + 4 * t) * DH + 32 * c + 8 * g;
+                kf[t][0] = ldg16(src);
+                kf[t][1] = ldg16(src + a.kv_plane);
+            }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int key = k0 + 8 * g + 2 * e;
-                    uint32_t w = vf[dt][e];
-                    if (key >= a.T) w &= 0xFFFF0000u;
-                    if (key + 1 >= a.T) w &= 0x0000FFFFu;
-                    vf[dt][e] = w;
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int u = 0; u < QT; ++u) {
+                    sacc[t][u] = mfma_bf16(kf[t][0], qf[u][c][0], sacc[t][u]);
+                    sacc[t][u] = mfma_bf16(kf[t][0], qf[u][c][1], sacc[t][u]);
+                    sacc[t][u] = mfma_bf16(kf[t][1], qf[u][c][0], sacc[t][u]);
                 }
         }
 
+        u32x4_t pf[QT][2];
 #pragma unroll
-        for (int t = 0; t < QT; ++t) {
-            f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int c = 0; c < NC; ++c) {
-                s0 = mfma_bf16(kf[0][c], qf[t][c], s0);
-                s1 = mfma_bf16(kf[1][c], qf[t][c], s1);
-            }
+        for (int u = 0; u < QT; ++u) {
             float sv[8];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int key0 = k0 + 8 * g + i, key1 = key0 + 4;
-                sv[i] = (key0 < lim[t]) ? s0[i] * sl2 : -INFINITY;
-                sv[4 + i] = (key1 < lim[t]) ? s1[i] * sl2 : -INFINITY;
+                sv[i] = (key0 < lim[u]) ? sacc[0][u][i] * sl2 : -INFINITY;
+                sv[4 + i] = (key1 < lim[u]) ? sacc[1][u][i] * sl2 : -INFINITY;
             }
             float bm = sv[0];
 #pragma unroll
             for (int j = 1; j < 8; ++j) bm = fmaxf(bm, sv[j]);
             bm = fmaxf(bm, __shfl_xor(bm, 16));
             bm = fmaxf(bm, __shfl_xor(bm, 32));
-            const float mnew = fmaxf(mrun[t], bm);
+            const float mnew = fmaxf(mrun[u], bm);
             float alpha = 1.f, ps = 0.f;
-            uint32_t pk[4];
-            if (mnew == -INFINITY) {
+            uint32_t phi[4] = {0u, 0u, 0u, 0u}, plo[4] = {0u, 0u, 0u, 0u};
+            if (mnew != -INFINITY) {
+                alpha = exp2f(mrun[u] - mnew);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) pk[e] = 0u;
-            } else {
-                alpha = exp2f(mrun[t] - mnew);
-                float p[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) { p[j] = exp2f(sv[j] - mnew); ps += p[j]; }
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    pk[e] = (uint32_t)f32_to_bf16(p[2 * e]) | ((uint32_t)f32_to_bf16(p[2 * e + 1]) << 16);
+                for (int e = 0; e < 4; ++e) {
+                    const float p0 = exp2f(sv[2 * e] - mnew), p1 = exp2f(sv[2 * e + 1] - mnew);
+                    ps += p0 + p1;
+                    uint16_t h0, l0, h1, l1;
+                    split_bf16(p0, h0, l0);
+                    split_bf16(p1, h1, l1);
+                    phi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+                    plo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+                }
             }
-            lrun[t] = lrun[t] * alpha + ps;
-            mrun[t] = mnew;
-            const u32x4_t pf = {pk[0], pk[1], pk[2], pk[3]};
+            lrun[u] = lrun[u] * alpha + ps;
+            mrun[u] = mnew;
+            pf[u][0] = u32x4_t{phi[0], phi[1], phi[2], phi[3]};
+            pf[u][1] = u32x4_t{plo[0], plo[1], plo[2], plo[3]};
 #pragma unroll
-            for (int dt = 0; dt < ND; ++dt) {
+            for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) oacc[dt][t][i] *= alpha;
-                oacc[dt][t] = mfma_bf16(vf[dt], pf, oacc[dt][t]);
+                for (int i = 0; i < 4; ++i) oacc[dt][u][i] *= alpha;
+        }
+
+        // O^T += V^T * P^T
+        const bool tail = (k0 + 8 * g + 8 > a.T);
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+            const uint16_t* src = Vp + (size_t)(16 * dt + r) * a.Cs + k0 + 8 * g;
+            u32x4_t vh = ldg16(src), vl = ldg16(src + a.kv_plane);
+            if (tail) {                        // zero V beyond T (those rows may be unwritten)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int key = k0 + 8 * g + 2 * e;
+                    uint32_t keep = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
+                    vh[e] &= keep;
+                    vl[e] &= keep;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < QT; ++u) {
+                oacc[dt][u] = mfma_bf16(vh, pf[u][0], oacc[dt][u]);
+                oacc[dt][u] = mfma_bf16(vh, pf[u][1], oacc[dt][u]);
+                oacc[dt][u] = mfma_bf16(vl, pf[u][0], oacc[dt][u]);
             }
         }
     }

@@ -43,9 +43,14 @@ template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { re
 //   f32  (KC = 16): lane l float s = row l%16, col 4s + g (s = 0..3, one MFMA each)
 //   int8 (KC = 64): lane l byte 8h + e = row l%16, col 32h + 8g + e (h = 0..1)
 // Packed weights: chunk (nt, kc) at byte ((nt * KCn + kc) * 64 + lane) * 16.
-// Activation fragments use the same chunk shape with rows = tokens; their chunk
-// width is 32 (bf16) or 16 (f32) columns:
-//   chunk (mt, kcx) at byte ((mt * KCx + kcx) * 64 + lane) * 16.
+//
+// Activation fragments use the same chunk shape with rows = tokens.  For fp32
+// models a chunk holds 16 fp32 columns.  For bf16 / int8-weight models a value v
+// is carried as two bf16 planes, hi = bf16(v) and lo = bf16(v - hi), so that the
+// A operand keeps ~16 significant bits; a chunk is then 32 columns, hi plane
+// (1 KiB) followed by lo plane (1 KiB), and the GEMM issues one MFMA per plane.
+//   fp32:  chunk (mt, kcx) at byte (mt * KCx + kcx) * 1024
+//   hi/lo: chunk (mt, kcx) at byte (mt * KCx + kcx) * 2048 (+1024 for lo)
 // ---------------------------------------------------------------------------
 
 template <int WT> struct WTraits;
@@ -53,29 +58,33 @@ template <> struct WTraits<WT_F32> { static constexpr int KC = 16; static conste
 template <> struct WTraits<WT_BF16> { static constexpr int KC = 32; static constexpr int XPER = 1; };
 template <> struct WTraits<WT_I8> { static constexpr int KC = 64; static constexpr int XPER = 2; };
 
-// Columns per activation chunk: 16 for fp32 activations, 32 for bf16.
-template <int WT> struct XCols { static constexpr int v = (WT == WT_F32) ? 16 : 32; };
+// Bytes of one activation chunk.
+template <bool F32> struct XChunk { static constexpr int bytes = F32 ? 1024 : 2048; };
 
-// Byte offset of activation element (m, k) in the fragment buffer with KCx chunks per tile row.
+// hi / lo bf16 split of an fp32 value.
+__device__ __forceinline__ void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
+    hi = f32_to_bf16(v);
+    lo = f32_to_bf16(v - bf16_to_f32(hi));
+}
+
+// Store activation element (m, k) into the fragment buffer with KCx chunks per tile row.
 template <bool F32>
-__device__ __forceinline__ size_t xfrag_offset(int m, int k, int KCx) {
+__device__ __forceinline__ void xfrag_store(void* base, int m, int k, int KCx, float v) {
     const int mt = m >> 4, r = m & 15;
     if (F32) {
         const int kc = k >> 4, kk = k & 15;
         const int g = kk & 3, s = kk >> 2;
-        return ((size_t)(mt * KCx + kc) * 64 + (r + 16 * g)) * 16 + s * 4;
+        char* p = (char*)base + ((size_t)(mt * KCx + kc) * 64 + (r + 16 * g)) * 16 + s * 4;
+        *(float*)p = v;
     } else {
         const int kc = k >> 5, kk = k & 31;
         const int g = kk >> 3, e = kk & 7;
-        return ((size_t)(mt * KCx + kc) * 64 + (r + 16 * g)) * 16 + e * 2;
+        char* p = (char*)base + (size_t)(mt * KCx + kc) * 2048 + (r + 16 * g) * 16 + e * 2;
+        uint16_t hi, lo;
+        split_bf16(v, hi, lo);
+        *(uint16_t*)p = hi;
+        *(uint16_t*)(p + 1024) = lo;
     }
-}
-
-template <bool F32>
-__device__ __forceinline__ void xfrag_store(void* base, int m, int k, int KCx, float v) {
-    char* p = (char*)base + xfrag_offset<F32>(m, k, KCx);
-    if (F32) *(float*)p = v;
-    else *(uint16_t*)p = f32_to_bf16(v);
 }
 
 __device__ __forceinline__ f32x4_t mfma_bf16(const u32x4_t& a, const u32x4_t& b, f32x4_t c) {

@@ -72,6 +72,7 @@ struct Workspace {
     LmPartial* lm = nullptr; // [n_lm_wg][wrows]
     float* opart = nullptr;  // [MAX_SPLIT][wrows][H][Dh]
     float* mlpart = nullptr; // [MAX_SPLIT][wrows][H][2]
+    size_t xg_bytes = 0, of_bytes = 0, af_bytes = 0;   // allocated fragment-buffer sizes
 };
 
 constexpr int MAX_SPLIT = 16;
@@ -82,7 +83,7 @@ struct dllm_model {
     dllm_config cfg;
     int wt = 0;              // WT_F32 / WT_BF16 / WT_I8
     bool xf32 = false;       // activations in fp32
-    size_t act_size = 2;     // bytes of one activation / KV element
+    size_t kv_elem = 4;      // bytes per cached K or V value (fp32, or a bf16 hi/lo pair)
     int KCx_d = 0, KCx_f = 0;
     std::vector<LayerW> layers;
     PackedW lm;
@@ -139,18 +140,18 @@ int pick_MT(int M) {
     return 4;
 }
 
-template <int WT, int F, int MT, int NW, int D, bool RSTD, class Epi>
+template <int WT, int F, int MT, int NW, bool RSTD, class Epi>
 void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
-    hipLaunchKernelGGL((gemm_kernel<WT, F, MT, NW, D, RSTD, Epi>), dim3(gx, gy), dim3((NW + (RSTD ? 1 : 0)) * 64),
+    hipLaunchKernelGGL((gemm_kernel<WT, F, MT, NW, RSTD, Epi>), dim3(gx, gy), dim3((NW + (RSTD ? 1 : 0)) * 64),
                        0, s, g, epi);
 }
 
-template <int WT, int F, int NW, int D, bool RSTD, class Epi>
+template <int WT, int F, int NW, bool RSTD, class Epi>
 int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
     switch (MT) {
-        case 1: launch_gemm_inst<WT, F, 1, NW, D, RSTD>(g, epi, gx, gy, s); break;
-        case 2: launch_gemm_inst<WT, F, 2, NW, D, RSTD>(g, epi, gx, gy, s); break;
-        case 4: launch_gemm_inst<WT, F, 4, NW, D, RSTD>(g, epi, gx, gy, s); break;
+        case 1: launch_gemm_inst<WT, F, 1, NW, RSTD>(g, epi, gx, gy, s); break;
+        case 2: launch_gemm_inst<WT, F, 2, NW, RSTD>(g, epi, gx, gy, s); break;
+        case 4: launch_gemm_inst<WT, F, 4, NW, RSTD>(g, epi, gx, gy, s); break;
         default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
     }
     return DLLM_OK;
@@ -159,17 +160,17 @@ int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hi
 template <int WT, GemmKind KIND, class Epi>
 int launch_gemm(int F, int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
     if constexpr (KIND == G_QKV) {
-        if (F == 3) return launch_gemm_mt<WT, 3, 4, 4, true>(MT, g, epi, gx, gy, s);
-        return launch_gemm_mt<WT, 1, 4, 8, true>(MT, g, epi, gx, gy, s);
+        if (F == 3) return launch_gemm_mt<WT, 3, 4, true>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 4, true>(MT, g, epi, gx, gy, s);
     } else if constexpr (KIND == G_GU) {
-        if (F == 6) return launch_gemm_mt<WT, 6, 4, 2, true>(MT, g, epi, gx, gy, s);
-        return launch_gemm_mt<WT, 1, 4, 8, true>(MT, g, epi, gx, gy, s);
+        if (F == 6) return launch_gemm_mt<WT, 6, 4, true>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 4, true>(MT, g, epi, gx, gy, s);
     } else if constexpr (KIND == G_LM) {
-        if (F == 8) return launch_gemm_mt<WT, 8, 4, 2, true>(MT, g, epi, gx, gy, s);
-        if (F == 4) return launch_gemm_mt<WT, 4, 4, 2, true>(MT, g, epi, gx, gy, s);
-        return launch_gemm_mt<WT, 1, 4, 8, true>(MT, g, epi, gx, gy, s);
+        if (F == 8) return launch_gemm_mt<WT, 8, 4, true>(MT, g, epi, gx, gy, s);
+        if (F == 4) return launch_gemm_mt<WT, 4, 4, true>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 4, true>(MT, g, epi, gx, gy, s);
     } else {
-        return launch_gemm_mt<WT, 1, 8, 8, false>(MT, g, epi, gx, gy, s);
+        return launch_gemm_mt<WT, 1, 8, false>(MT, g, epi, gx, gy, s);
     }
 }
 
@@ -227,10 +228,13 @@ int ensure_ws(dllm_model* m, int rows_needed) {
 #define ALLOC(ptr, bytes) \
     if ((rc = alloc_zero((void**)&(ptr), (bytes))) != DLLM_OK) { free_ws(w); return rc; }
     ALLOC(w.x, (size_t)rows * d * 4);
-    ALLOC(w.xg, (size_t)(rows / 16) * m->KCx_d * 1024);
-    ALLOC(w.q, (size_t)rows * d * m->act_size);
-    ALLOC(w.of, (size_t)(rows / 16) * m->KCx_d * 1024);
-    ALLOC(w.af, (size_t)(rows / 16) * m->KCx_f * 1024);
+    const size_t xchunk = m->xf32 ? 1024 : 2048;   // an activation chunk: fp32, or bf16 hi + lo
+    w.xg_bytes = w.of_bytes = (size_t)(rows / 16) * m->KCx_d * xchunk;
+    w.af_bytes = (size_t)(rows / 16) * m->KCx_f * xchunk;
+    ALLOC(w.xg, w.xg_bytes);
+    ALLOC(w.q, (size_t)rows * d * 4);   // fp32, or bf16 hi and lo planes
+    ALLOC(w.of, w.of_bytes);
+    ALLOC(w.af, w.af_bytes);
     ALLOC(w.ssq, (size_t)m->n_part_max * rows * 4);
     ALLOC(w.pos, (size_t)rows * 4);
     ALLOC(w.lim, (size_t)rows * 4);
@@ -317,7 +321,7 @@ struct FwdArgs {
     float* xout;              // residual copy or nullptr
 };
 
-template <int WT, typename AT>
+template <int WT, typename AT>   // AT: element type of the embedding and the cache planes
 int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     constexpr bool XF32 = (WT == WT_F32);
     const dllm_config& c = m->cfg;
@@ -330,22 +334,34 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     if (a.M <= 64) { MT = pick_MT(a.M); gy = 1; }
     else { MT = 4; gy = ceil_div(a.M, 64); }
     const int Mc = gy * MT * 16;    // rows computed (padded)
+    // Every kernel below touches token rows [0, Mc) of the workspace buffers.
+    {
+        const size_t need_d = (size_t)(Mc / 16) * m->KCx_d * XChunk<XF32>::bytes;
+        const size_t need_f = (size_t)(Mc / 16) * m->KCx_f * XChunk<XF32>::bytes;
+        if (Mc > w.rows || need_d > w.xg_bytes || need_d > w.of_bytes || need_f > w.af_bytes)
+            return fail(DLLM_E_INVAL, "internal: workspace smaller than the launch extent");
+        if (a.lm && Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
+    }
 
     hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(256), 0, s, (const AT*)m->embed, a.tok, a.mask, a.M,
                        d, c.vocab, c.mask_id, (const float*)m->layers[0].g1, w.x, w.xg, m->KCx_d, w.ssq);
     int n_part = 1;
 
-    const size_t layer_elems = (size_t)2 * H * kv->Cs * Dh;
+    // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo].
+    const size_t plane = (size_t)H * kv->Cs * Dh;
+    const size_t layer_elems = (XF32 ? 2 : 4) * plane;
+    const size_t kv_plane = XF32 ? 0 : plane;
+    const size_t q_plane = XF32 ? 0 : (size_t)w.rows * d;
     for (int l = 0; l < a.n_layers; ++l) {
         LayerW& L = m->layers[l];
         AT* Kc = (AT*)kv->buf + (size_t)l * layer_elems;
-        AT* Vt = Kc + (size_t)H * kv->Cs * Dh;
+        AT* Vt = Kc + (XF32 ? plane : 2 * plane);
 
         // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
         {
             GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles,
                        w.ssq, n_part, w.rows, 1.0f / d, c.eps};
-            EpiQKV<AT> e{d, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, Kc, Vt, kv->Cs};
+            EpiQKV<XF32> e{d, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane, kv->Cs};
             const int F = pick_F(G_QKV, L.qkv.n_tiles, MT);
             ProbeScope ps(m, DLLM_K_QKV, s);
             if ((rc = launch_gemm<WT, G_QKV>(F, MT, g, e, ceil_div(L.qkv.n_tiles, F), gy, s))) return rc;
@@ -353,7 +369,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         // attention over [0, T) (+ split merge)
         {
             AttnArgs at{};
-            at.q = w.q; at.K = Kc; at.Vt = Vt; at.Cs = kv->Cs; at.H = H; at.T = a.T; at.lim = a.lim; at.M = a.M;
+            at.q = w.q; at.q_plane = q_plane; at.K = Kc; at.Vt = Vt; at.kv_plane = kv_plane; at.Cs = kv->Cs; at.H = H; at.T = a.T; at.lim = a.lim; at.M = a.M;
             at.scale = 1.0f / sqrtf((float)Dh); at.o = w.of; at.KCx = m->KCx_d;
             at.opart = w.opart; at.mlpart = w.mlpart; at.rows_ld = w.wrows;
             ProbeScope ps(m, DLLM_K_ATTN, s);
@@ -363,7 +379,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 else if (Dh == 64) hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(Mc, H), dim3(64), 0, s, at);
                 else hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(Mc, H), dim3(64), 0, s, at);
             } else {
-                const int QT = (a.M <= 64) ? MT : 4;
+                const int QT = (a.M <= 16) ? 1 : 2;
                 const int nqb = ceil_div(Mc, 16 * QT);
                 const int nblk = ceil_div(a.T, 32);
                 int nsplit = 1;
@@ -376,9 +392,9 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 dim3 grid(at.nsplit, H, nqb);
 #define ATTN(DH_, QT_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, QT_>), grid, dim3(64), 0, s, at)
                 if (Dh == 128) {
-                    if (QT == 1) ATTN(128, 1); else if (QT == 2) ATTN(128, 2); else ATTN(128, 4);
+                    if (QT == 1) ATTN(128, 1); else ATTN(128, 2);
                 } else {
-                    if (QT == 1) ATTN(64, 1); else if (QT == 2) ATTN(64, 2); else ATTN(64, 4);
+                    if (QT == 1) ATTN(64, 1); else ATTN(64, 2);
                 }
 #undef ATTN
                 if (at.nsplit > 1) {
@@ -479,7 +495,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     const dllm_config& c = m->cfg;
     m->wt = c.dtype == DLLM_F32 ? WT_F32 : (c.dtype == DLLM_BF16 ? WT_BF16 : WT_I8);
     m->xf32 = c.dtype == DLLM_F32;
-    m->act_size = m->xf32 ? 4 : 2;
+    m->kv_elem = 4;
     const int xcols = m->xf32 ? 16 : 32;
     const int xper = m->wt == WT_I8 ? 2 : 1;
     const int d = c.d_model, F = c.d_ff;
@@ -582,7 +598,7 @@ int dllm_kv_bytes(const dllm_model* m, int32_t capacity, size_t* bytes) {
     if (capacity < 1 || capacity > m->cfg.max_pos)
         return fail(DLLM_E_CAPACITY, "capacity must be in [1, max_pos]");
     const dllm_config& c = m->cfg;
-    *bytes = (size_t)c.n_layers * 2 * c.n_heads * cs_of(capacity) * c.head_dim * m->act_size;
+    *bytes = (size_t)c.n_layers * 2 * c.n_heads * cs_of(capacity) * c.head_dim * m->kv_elem;
     return DLLM_OK;
 }
 
@@ -771,7 +787,7 @@ int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int3
     if (!m || !bytes) return fail(DLLM_E_INVAL, "NULL argument");
     const dllm_config& c = m->cfg;
     const double wsz = m->wt == WT_F32 ? 4.0 : (m->wt == WT_BF16 ? 2.0 : 1.0);
-    const double asz = (double)m->act_size;
+    const double asz = (double)m->kv_elem;   // activations and cache values: 4 bytes
     const double d = c.d_model, F = c.d_ff, V = c.vocab;
     const double scale_b = (m->wt == WT_I8) ? 4.0 : 0.0;   // per weight row
     double b = 0;

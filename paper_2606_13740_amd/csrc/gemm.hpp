@@ -14,6 +14,8 @@
 // the K sum, so the A operand only carries x * g (rounded once).
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace dllm {
@@ -73,10 +75,23 @@ __device__ __forceinline__ void rstd_wave(const GemmArgs& g, int m0, int mcols, 
 // threads of the workgroup call it; scratch is LDS of at least nrows*ldy floats
 // that the epilogue may overwrite (it aliases Y).
 
-template <int WT, int F, int MT, int NW, int D, bool RSTD, class Epi>
+// Loads in flight per wave: as many K chunks as fit in ~128 VGPRs of buffers.
+template <int WT, int F, int MT>
+constexpr int pipeline_depth() {
+    constexpr int XP = (WT == WT_F32) ? 1 : 2;
+    constexpr int slot = 4 * (F + MT * WTraits<WT>::XPER * XP);
+    constexpr int d = 128 / slot;
+    return d < 1 ? 1 : (d > 8 ? 8 : d);
+}
+
+template <int WT, int F, int MT, int NW, bool RSTD, class Epi>
 __global__ void __launch_bounds__((NW + (RSTD ? 1 : 0)) * 64)
 gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int XPER = WTraits<WT>::XPER;
+    constexpr bool XF = (WT == WT_F32);
+    constexpr int XP = XF ? 1 : 2;                 // activation planes (hi, lo)
+    constexpr int XB = XChunk<XF>::bytes;
+    constexpr int D = pipeline_depth<WT, F, MT>();
     constexpr int NR = 16 * F, MR = 16 * MT, LDY = MR + 1;
     __shared__ float Y[NR * LDY];
     __shared__ float rstd_lds[64];
@@ -98,11 +113,11 @@ gemm_kernel(GemmArgs g, Epi epi) {
         const int c0 = (int)(((long)wave * g.KCw) / NW);
         const int c1 = (int)(((long)(wave + 1) * g.KCw) / NW);
         const char* wp = (const char*)g.W + ((size_t)nt0 * g.KCw * 64 + lane) * 16;
-        const char* xp = (const char*)g.X + ((size_t)mt0 * g.KCx * 64 + lane) * 16;
-        const size_t wtile = (size_t)g.KCw * 1024, xtile = (size_t)g.KCx * 1024;
+        const char* xp = (const char*)g.X + (size_t)mt0 * g.KCx * XB + lane * 16;
+        const size_t wtile = (size_t)g.KCw * 1024, xtile = (size_t)g.KCx * XB;
 
         u32x4_t wb[D][F];
-        u32x4_t xb[D][MT * XPER];
+        u32x4_t xb[D][MT * XPER * XP];
 
         auto load = [&](int s, int c) {
 #pragma unroll
@@ -112,7 +127,10 @@ gemm_kernel(GemmArgs g, Epi epi) {
             for (int t = 0; t < MT; ++t)
 #pragma unroll
                 for (int h = 0; h < XPER; ++h)
-                    xb[s][t * XPER + h] = ldg16(xp + t * xtile + (size_t)(c * XPER + h) * 1024);
+#pragma unroll
+                    for (int pl = 0; pl < XP; ++pl)
+                        xb[s][(t * XPER + h) * XP + pl] =
+                            ldg16(xp + t * xtile + (size_t)(c * XPER + h) * XB + pl * 1024);
         };
         auto compute = [&](int s) {
 #pragma unroll
@@ -120,14 +138,19 @@ gemm_kernel(GemmArgs g, Epi epi) {
                 if (f >= nf) continue;
                 if constexpr (WT == WT_BF16) {
 #pragma unroll
-                    for (int t = 0; t < MT; ++t) acc[f][t] = mfma_bf16(wb[s][f], xb[s][t], acc[f][t]);
+                    for (int t = 0; t < MT; ++t) {
+                        acc[f][t] = mfma_bf16(wb[s][f], xb[s][t * 2 + 0], acc[f][t]);
+                        acc[f][t] = mfma_bf16(wb[s][f], xb[s][t * 2 + 1], acc[f][t]);
+                    }
                 } else if constexpr (WT == WT_I8) {
                     const u32x4_t w0 = i8x8_to_bf16x8(wb[s][f][0], wb[s][f][1]);
                     const u32x4_t w1 = i8x8_to_bf16x8(wb[s][f][2], wb[s][f][3]);
 #pragma unroll
                     for (int t = 0; t < MT; ++t) {
-                        acc[f][t] = mfma_bf16(w0, xb[s][t * 2 + 0], acc[f][t]);
-                        acc[f][t] = mfma_bf16(w1, xb[s][t * 2 + 1], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w0, xb[s][(t * 2 + 0) * 2 + 0], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w0, xb[s][(t * 2 + 0) * 2 + 1], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w1, xb[s][(t * 2 + 1) * 2 + 0], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w1, xb[s][(t * 2 + 1) * 2 + 1], acc[f][t]);
                     }
                 } else {
 #pragma unroll
@@ -198,17 +221,32 @@ gemm_kernel(GemmArgs g, Epi epi) {
 // Q/K/V projection: RoPE on Q and K, Q to a row-major buffer, K and V to the
 // cache at each token's position.  Packed rows: [Q | K | V], each d rows; inside
 // a Q or K head, packed row 2i is dim i and row 2i+1 is dim i + Dh/2, so a RoPE
-// pair is two adjacent rows.
-template <typename T>
+// pair is two adjacent rows.  fp32 models store one fp32 plane; bf16 / int8
+// models store a hi and a lo bf16 plane (`plane` elements apart).
+template <bool XF32>
 struct EpiQKV {
+    using T = typename std::conditional<XF32, float, uint16_t>::type;
     int d, Dh, M;
     int pos_base;           // position of token m is pos ? pos[m] : pos_base + m
     const int* pos;
     const float2* rope;     // [max_pos][Dh/2] (cos, sin)
-    T* q;                   // [rows][d]
-    T* Kc;                  // layer base of K   [H][Cs][Dh]
-    T* Vt;                  // layer base of V^T [H][Dh][Cs]
+    T* q;                   // [rows][d] (+ lo plane at q + q_plane)
+    size_t q_plane;
+    T* Kc;                  // layer base of K   [H][Cs][Dh] (+ lo plane at kv_plane)
+    T* Vt;                  // layer base of V^T [H][Dh][Cs] (+ lo plane at kv_plane)
+    size_t kv_plane;
     int Cs;
+
+    __device__ __forceinline__ static void put(T* p, size_t plane, float v) {
+        if constexpr (XF32) {
+            *p = v;
+        } else {
+            uint16_t hi, lo;
+            split_bf16(v, hi, lo);
+            p[0] = hi;
+            p[plane] = lo;
+        }
+    }
 
     __device__ void operator()(const float* Y, int ldy, int n0, int nrows, int m0, int mcols) const {
         const int npairs = nrows >> 1;
@@ -229,17 +267,17 @@ struct EpiQKV {
                 const float rb = a * cs.y + b * cs.x;
                 if (seg == 0) {
                     T* dst = q + (size_t)m * d + h * Dh;
-                    dst[j] = from_f32<T>(ra);
-                    dst[j + half] = from_f32<T>(rb);
+                    put(dst + j, q_plane, ra);
+                    put(dst + j + half, q_plane, rb);
                 } else {
                     T* dst = Kc + ((size_t)h * Cs + ps) * Dh;
-                    dst[j] = from_f32<T>(ra);
-                    dst[j + half] = from_f32<T>(rb);
+                    put(dst + j, kv_plane, ra);
+                    put(dst + j + half, kv_plane, rb);
                 }
             } else {
                 T* dst = Vt + ((size_t)h * Dh + rr) * Cs + ps;
-                dst[0] = from_f32<T>(a);
-                dst[Cs] = from_f32<T>(b);
+                put(dst, kv_plane, a);
+                put(dst + Cs, kv_plane, b);
             }
         }
     }

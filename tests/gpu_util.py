@@ -68,6 +68,7 @@ def assert_logits_close(got, ref, atol):
     fin = np.isfinite(ref)
     assert np.array_equal(fin, np.isfinite(got)), "MASK column must be -inf on both sides"
     err = float(np.max(np.abs(got[fin] - ref[fin])))
+    print(f"  max |dlogit| = {err:.3e} (tolerance {atol:.1e})", flush=True)
     assert err <= atol, f"max |dlogit| = {err:.3e} > {atol:.1e}"
     return err
 

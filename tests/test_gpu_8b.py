@@ -1,0 +1,65 @@
+"""Full-width parity at the LLaDA-8B shape (d 4096, 32 heads x 128, FFN 12288,
+vocab 126464) in the launch configuration the benchmark times.
+
+The kernels' launch shapes depend only on the widths and the window size, so
+the 2-layer cases exercise exactly the benchmark's GEMM, attention and LM-head
+launches; the full 32-layer case compares one whole step at prefix 512 with
+the oracle (it takes about a minute of CPU time on the host).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import assert_ids_match_where_decided, assert_logits_close, dev_i32, gpu_logits, gpu_step, tol
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2606_13740_amd as dl  # noqa: E402
+
+BIG = synth.LLADA_8B
+
+
+def _run(shape, dtype, P, W, masked, cap_extra=0):
+    print(f"case: 8B-width {dtype}, layers {shape.n_layers}, prefix {P}, window {W}", flush=True)
+    layers = [synth.layer_weights(shape, l, "bf16") for l in range(shape.n_layers)]
+    glob = synth.global_weights(shape, "bf16")
+    model = dl.Model(shape, dtype, glob, lambda l: layers[l], max_window=64, max_pos=P + W + 64)
+    kv = dl.KVCache(model, P + W + cap_extra)
+    prompt = synth.prompt_ids(shape, P)
+    dl.dllm_prefill(model.handle, kv.handle, dev_i32(prompt), P)
+    tok, mask = synth.window(shape, W, masked)
+    logits, ids, conf = gpu_logits(model, kv, tok, mask)
+    s_ids, s_conf = gpu_step(model, kv, tok, mask)
+    print("  gpu done; oracle ...", flush=True)
+    om = oracle.OracleModel(shape, dict(glob, layers=layers), int8=(dtype == "w8"), cache_layers=False)
+    okv = oracle.OracleKV(shape, P + W + cap_extra)
+    oracle.prefill(om, okv, prompt)
+    ref = oracle.denoise_step(om, okv, tok, mask)
+    err = assert_logits_close(logits, ref.logits, tol(dtype))
+    frac = assert_ids_match_where_decided(ids, ref.logits, err)
+    print(f"  max |dlogit| = {err:.3e}; argmax decided on {frac:.0%} of rows", flush=True)
+    np.testing.assert_array_equal(s_ids, ids)
+    np.testing.assert_array_equal(s_conf, conf)
+    np.testing.assert_allclose(conf, ref.conf, rtol=0.2)
+    assert np.all(ids != shape.mask_id) and np.all((conf > 0) & (conf <= 1))
+    kv.close()
+    model.close()
+    return err
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("dtype,P,W", [("bf16", 512, 32), ("bf16", 1024, 64), ("w8", 512, 64)])
+def test_8b_width_two_layers(dtype, P, W):
+    masked = list(range(8, 32)) if W == 32 else list(range(24, 64))
+    _run(BIG.with_layers(2), dtype, P, W, masked)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_8b_full_depth_step():
+    _run(BIG, "bf16", 512, 32, list(range(8, 32)))
