@@ -41,20 +41,38 @@ struct AttnArgs {
 // bf16 MFMA path.  Q, K and V are carried as hi + lo bf16 planes and each
 // product takes three MFMAs (hi*hi + hi*lo + lo*hi), so scores and outputs keep
 // ~16 significant bits; the probabilities P are split the same way.
-template <int DH, int QT>
-__global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
+//
+// Workgroup = (split, head, query block of 16*QT rows) with NWA waves; the
+// split's 32-key blocks are dealt out to the waves in contiguous runs, each
+// wave keeps its own online softmax, and the waves are merged in LDS (max over
+// waves, then the rescaled outputs summed wave by wave in a fixed order).  With
+// one split the normalised output goes straight to the O projection's
+// fragments; otherwise (m, l, o) per split goes to attn_combine.
+template <int DH, int QT, int NWA>
+__global__ void __launch_bounds__(NWA * 64) attn_bf16_kernel(AttnArgs a) {
     constexpr int NC = DH / 32;     // 32-dim chunks
     constexpr int ND = DH / 16;     // 16-dim output tiles
-    const int lane = threadIdx.x;
+    constexpr int NQ = 16 * QT;     // query rows of the workgroup
+    __shared__ float mx_s[NWA][NQ];
+    __shared__ float l_s[NWA][NQ];
+    __shared__ float obuf[NQ][DH + 1];
+    __shared__ float Mq[NQ], Lq[NQ];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, h = blockIdx.y;
-    const int row0 = blockIdx.z * 16 * QT;
+    const int row0 = blockIdx.z * NQ;
     const int ld = a.H * DH;
     const float sl2 = a.scale * 1.4426950408889634f;
 
     const uint16_t* qp = (const uint16_t*)a.q;
     const uint16_t* Kp = (const uint16_t*)a.K + (size_t)h * a.Cs * DH;
     const uint16_t* Vp = (const uint16_t*)a.Vt + (size_t)h * DH * a.Cs;
+
+    const int nblk = (a.T + 31) >> 5;
+    const int sb0 = split * a.bps, sb1 = min(nblk, sb0 + a.bps);
+    const int kb0 = sb0 + (int)(((long)wave * (sb1 - sb0)) / NWA);
+    const int kb1 = sb0 + (int)(((long)(wave + 1) * (sb1 - sb0)) / NWA);
 
     u32x4_t qf[QT][NC][2];
     int lim[QT];
@@ -80,13 +98,28 @@ __global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
         for (int dt = 0; dt < ND; ++dt) oacc[dt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int nblk = (a.T + 31) >> 5;
-    const int kb0 = split * a.bps;
-    const int kb1 = min(nblk, kb0 + a.bps);
     const int krow0 = 8 * (r >> 2) + (r & 3);   // + 4t: the key this lane loads for tile t
 
     for (int kb = kb0; kb < kb1; ++kb) {
         const int k0 = kb * 32;
+        // issue the block's K and V loads together
+        u32x4_t kf[NC][2][2];
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const uint16_t* src = Kp + (size_t)(k0 + krow0 + 4 * t) * DH + 32 * c + 8 * g;
+                kf[c][t][0] = ldg16(src);
+                kf[c][t][1] = ldg16(src + a.kv_plane);
+            }
+        u32x4_t vf[ND][2];
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+            const uint16_t* src = Vp + (size_t)(16 * dt + r) * a.Cs + k0 + 8 * g;
+            vf[dt][0] = ldg16(src);
+            vf[dt][1] = ldg16(src + a.kv_plane);
+        }
+
         // scores S^T for both 16-key tiles and every query tile
         f32x4_t sacc[2][QT];
 #pragma unroll
@@ -94,23 +127,15 @@ __global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
             for (int u = 0; u < QT; ++u) sacc[t][u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            u32x4_t kf[2][2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                const uint16_t* src = Kp + (size_t)(k0 + krow0 + 4 * t) * DH + 32 * c + 8 * g;
-                kf[t][0] = ldg16(src);
-                kf[t][1] = ldg16(src + a.kv_plane);
-            }
+        for (int c = 0; c < NC; ++c)
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int u = 0; u < QT; ++u) {
-                    sacc[t][u] = mfma_bf16(kf[t][0], qf[u][c][0], sacc[t][u]);
-                    sacc[t][u] = mfma_bf16(kf[t][0], qf[u][c][1], sacc[t][u]);
-                    sacc[t][u] = mfma_bf16(kf[t][1], qf[u][c][0], sacc[t][u]);
+                    sacc[t][u] = mfma_bf16(kf[c][t][0], qf[u][c][0], sacc[t][u]);
+                    sacc[t][u] = mfma_bf16(kf[c][t][0], qf[u][c][1], sacc[t][u]);
+                    sacc[t][u] = mfma_bf16(kf[c][t][1], qf[u][c][0], sacc[t][u]);
                 }
-        }
 
         u32x4_t pf[QT][2];
 #pragma unroll
@@ -154,53 +179,80 @@ __global__ void __launch_bounds__(64) attn_bf16_kernel(AttnArgs a) {
         }
 
         // O^T += V^T * P^T
-        const bool tail = (k0 + 8 * g + 8 > a.T);
+        if (k0 + 8 * g + 8 > a.T) {            // tail: zero V beyond T (those rows may be unwritten)
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) {
-            const uint16_t* src = Vp + (size_t)(16 * dt + r) * a.Cs + k0 + 8 * g;
-            u32x4_t vh = ldg16(src), vl = ldg16(src + a.kv_plane);
-            if (tail) {                        // zero V beyond T (those rows may be unwritten)
+            for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int key = k0 + 8 * g + 2 * e;
-                    uint32_t keep = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
-                    vh[e] &= keep;
-                    vl[e] &= keep;
+                    const uint32_t keep = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
+                    vf[dt][0][e] &= keep;
+                    vf[dt][1][e] &= keep;
                 }
-            }
+        }
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
             for (int u = 0; u < QT; ++u) {
-                oacc[dt][u] = mfma_bf16(vh, pf[u][0], oacc[dt][u]);
-                oacc[dt][u] = mfma_bf16(vh, pf[u][1], oacc[dt][u]);
-                oacc[dt][u] = mfma_bf16(vl, pf[u][0], oacc[dt][u]);
+                oacc[dt][u] = mfma_bf16(vf[dt][0], pf[u][0], oacc[dt][u]);
+                oacc[dt][u] = mfma_bf16(vf[dt][0], pf[u][1], oacc[dt][u]);
+                oacc[dt][u] = mfma_bf16(vf[dt][1], pf[u][0], oacc[dt][u]);
             }
-        }
     }
 
+    // ---- merge the NWA waves ----
 #pragma unroll
-    for (int t = 0; t < QT; ++t) {
-        float l = lrun[t];
+    for (int u = 0; u < QT; ++u) {
+        float l = lrun[u];
         l += __shfl_xor(l, 16);
         l += __shfl_xor(l, 32);
-        const int row = row0 + 16 * t + r;
-        if (a.nsplit == 1) {
-            const float inv = 1.f / l;
+        if (g == 0) {
+            mx_s[wave][16 * u + r] = mrun[u];
+            l_s[wave][16 * u + r] = l;
+        }
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < NQ; q += blockDim.x) {
+        float M = -INFINITY;
+        for (int w = 0; w < NWA; ++w) M = fmaxf(M, mx_s[w][q]);
+        float L = 0.f;
+        for (int w = 0; w < NWA; ++w)
+            if (mx_s[w][q] != -INFINITY) L += l_s[w][q] * exp2f(mx_s[w][q] - M);
+        Mq[q] = M;
+        Lq[q] = L;
+    }
+    __syncthreads();
+    for (int w = 0; w < NWA; ++w) {
+        if (wave == w) {
 #pragma unroll
-            for (int dt = 0; dt < ND; ++dt)
+            for (int u = 0; u < QT; ++u) {
+                const int q = 16 * u + r;
+                const float sc = (mrun[u] == -INFINITY) ? 0.f : exp2f(mrun[u] - Mq[q]);
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    xfrag_store<false>(a.o, row, h * DH + 16 * dt + 4 * g + i, a.KCx, oacc[dt][t][i] * inv);
-        } else {
-            float* op = a.opart + (((size_t)split * a.rows_ld + row) * a.H + h) * DH;
+                for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-            for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) op[16 * dt + 4 * g + i] = oacc[dt][t][i];
-            if (g == 0) {
-                float* ml = a.mlpart + (((size_t)split * a.rows_ld + row) * a.H + h) * 2;
-                ml[0] = mrun[t];
-                ml[1] = l;
+                    for (int i = 0; i < 4; ++i) {
+                        float* o = &obuf[q][16 * dt + 4 * g + i];
+                        *o = (w == 0 ? 0.f : *o) + oacc[dt][u][i] * sc;
+                    }
             }
+        }
+        __syncthreads();
+    }
+    if (a.nsplit == 1) {
+        for (int idx = threadIdx.x; idx < NQ * DH; idx += blockDim.x) {
+            const int q = idx / DH, dim = idx % DH;
+            xfrag_store<false>(a.o, row0 + q, h * DH + dim, a.KCx, obuf[q][dim] / Lq[q]);
+        }
+    } else {
+        for (int idx = threadIdx.x; idx < NQ * DH; idx += blockDim.x) {
+            const int q = idx / DH, dim = idx % DH;
+            a.opart[(((size_t)split * a.rows_ld + row0 + q) * a.H + h) * DH + dim] = obuf[q][dim];
+        }
+        for (int q = threadIdx.x; q < NQ; q += blockDim.x) {
+            float* ml = a.mlpart + (((size_t)split * a.rows_ld + row0 + q) * a.H + h) * 2;
+            ml[0] = Mq[q];
+            ml[1] = Lq[q];
         }
     }
 }

@@ -70,12 +70,15 @@ struct Workspace {
     int* pos = nullptr;      // [rows]
     int* lim = nullptr;      // [rows]
     LmPartial* lm = nullptr; // [n_lm_wg][wrows]
+    float* part = nullptr;   // split-K partials [KS][rows][d]
+    size_t part_floats = 0;
     float* opart = nullptr;  // [MAX_SPLIT][wrows][H][Dh]
     float* mlpart = nullptr; // [MAX_SPLIT][wrows][H][2]
     size_t xg_bytes = 0, of_bytes = 0, af_bytes = 0;   // allocated fragment-buffer sizes
 };
 
 constexpr int MAX_SPLIT = 16;
+constexpr int RES_SPLIT = 8;     // K slices of the O / down projections for windows of <= 64 rows
 
 }  // namespace
 
@@ -121,56 +124,70 @@ namespace {
 
 enum GemmKind { G_QKV = 0, G_RES = 1, G_GU = 2, G_LM = 3 };
 
-// Row tiles per workgroup: enough workgroups to cover 256 CUs, and few enough
-// registers that a 64-token tile does not spill.
-int pick_F(GemmKind k, int n_tiles, int MT) {
-    switch (k) {
-        case G_QKV: return n_tiles >= 256 * 3 ? 3 : 1;
-        case G_GU: return n_tiles >= 256 * 6 ? 6 : 1;
-        case G_LM:
-            if (n_tiles >= 256 * 8) return MT >= 4 ? 4 : 8;
-            return 1;
-        default: return 1;
-    }
-}
-
 int pick_MT(int M) {
     if (M <= 16) return 1;
     if (M <= 32) return 2;
     return 4;
 }
 
-template <int WT, int F, int MT, int NW, bool RSTD, class Epi>
-void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
-    hipLaunchKernelGGL((gemm_kernel<WT, F, MT, NW, RSTD, Epi>), dim3(gx, gy), dim3((NW + (RSTD ? 1 : 0)) * 64),
-                       0, s, g, epi);
+// Decompositions (measured on MI355X at the LLaDA-8B shapes, weights rotated
+// through >1 GB so that HBM is streamed):
+//   QKV    3 row tiles per workgroup, K split over 8 waves          (4.3 TB/s)
+//   gate/up 6 row tiles per workgroup, K split over 8 waves         (5.2 TB/s)
+//   LM head 4 waves x 8 row tiles, each wave streams the whole K    (6.3 TB/s)
+//   O/down 4 row tiles, K split over 4 waves x 8 workgroups (split-K) + reduction
+// Small models (fewer row tiles than CUs x tiles) use one tile per workgroup.
+bool big(GemmKind k, int n_tiles) {
+    switch (k) {
+        case G_QKV: return n_tiles >= 256 * 3;
+        case G_GU: return n_tiles >= 256 * 6;
+        case G_LM: return n_tiles >= 256 * 8;
+        default: return n_tiles >= 256;
+    }
 }
 
-template <int WT, int F, int NW, bool RSTD, class Epi>
-int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
+template <int WT, int FW, int NWn, int NWk, int MT, bool RSTD, class Epi>
+void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
+    dim3 grid(ceil_div(n_tiles, FW * NWn), KS, gy);
+    hipLaunchKernelGGL((gemm_kernel<WT, FW, NWn, NWk, MT, RSTD, Epi>), grid, dim3(NWn * NWk * 64), 0, s, g, epi);
+}
+
+template <int WT, int FW, int NWn, int NWk, bool RSTD, class Epi>
+int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
     switch (MT) {
-        case 1: launch_gemm_inst<WT, F, 1, NW, RSTD>(g, epi, gx, gy, s); break;
-        case 2: launch_gemm_inst<WT, F, 2, NW, RSTD>(g, epi, gx, gy, s); break;
-        case 4: launch_gemm_inst<WT, F, 4, NW, RSTD>(g, epi, gx, gy, s); break;
+        case 1: launch_gemm_inst<WT, FW, NWn, NWk, 1, RSTD>(g, epi, n_tiles, KS, gy, s); break;
+        case 2: launch_gemm_inst<WT, FW, NWn, NWk, 2, RSTD>(g, epi, n_tiles, KS, gy, s); break;
+        case 4: launch_gemm_inst<WT, FW, NWn, NWk, 4, RSTD>(g, epi, n_tiles, KS, gy, s); break;
         default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
     }
     return DLLM_OK;
 }
 
+// Number of row groups (partials) a launch writes.
+int row_groups(GemmKind k, int n_tiles) {
+    switch (k) {
+        case G_QKV: return big(k, n_tiles) ? ceil_div(n_tiles, 3) : n_tiles;
+        case G_GU: return big(k, n_tiles) ? ceil_div(n_tiles, 6) : n_tiles;
+        case G_LM: return big(k, n_tiles) ? ceil_div(n_tiles, 8) : n_tiles;
+        default: return big(k, n_tiles) ? ceil_div(n_tiles, 4) : n_tiles;
+    }
+}
+
 template <int WT, GemmKind KIND, class Epi>
-int launch_gemm(int F, int MT, const GemmArgs& g, const Epi& epi, int gx, int gy, hipStream_t s) {
+int launch_gemm(int n_tiles, int MT, int KS, const GemmArgs& g, const Epi& epi, int gy, hipStream_t s) {
+    const bool b = big(KIND, n_tiles);
     if constexpr (KIND == G_QKV) {
-        if (F == 3) return launch_gemm_mt<WT, 3, 4, true>(MT, g, epi, gx, gy, s);
-        return launch_gemm_mt<WT, 1, 4, true>(MT, g, epi, gx, gy, s);
+        if (b) return launch_gemm_mt<WT, 3, 1, 8, true>(MT, g, epi, n_tiles, 1, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4, true>(MT, g, epi, n_tiles, 1, gy, s);
     } else if constexpr (KIND == G_GU) {
-        if (F == 6) return launch_gemm_mt<WT, 6, 4, true>(MT, g, epi, gx, gy, s);
-        return launch_gemm_mt<WT, 1, 4, true>(MT, g, epi, gx, gy, s);
+        if (b) return launch_gemm_mt<WT, 6, 1, 8, true>(MT, g, epi, n_tiles, 1, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4, true>(MT, g, epi, n_tiles, 1, gy, s);
     } else if constexpr (KIND == G_LM) {
-        if (F == 8) return launch_gemm_mt<WT, 8, 4, true>(MT, g, epi, gx, gy, s);
-        if (F == 4) return launch_gemm_mt<WT, 4, 4, true>(MT, g, epi, gx, gy, s);
-        return launch_gemm_mt<WT, 1, 4, true>(MT, g, epi, gx, gy, s);
+        if (b) return launch_gemm_mt<WT, 8, 4, 1, true>(MT, g, epi, n_tiles, 1, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4, true>(MT, g, epi, n_tiles, 1, gy, s);
     } else {
-        return launch_gemm_mt<WT, 1, 8, false>(MT, g, epi, gx, gy, s);
+        if (b) return launch_gemm_mt<WT, 4, 1, 4, false>(MT, g, epi, n_tiles, KS, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4, false>(MT, g, epi, n_tiles, KS, gy, s);
     }
 }
 
@@ -199,7 +216,7 @@ struct ProbeScope {
 // ---------------------------------------------------------------------------
 
 void free_ws(Workspace& w) {
-    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.ssq, w.pos, w.lim, w.lm, w.opart, w.mlpart};
+    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.ssq, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     w = Workspace{};
@@ -239,6 +256,8 @@ int ensure_ws(dllm_model* m, int rows_needed) {
     ALLOC(w.pos, (size_t)rows * 4);
     ALLOC(w.lim, (size_t)rows * 4);
     ALLOC(w.lm, (size_t)m->n_lm_wg * w.wrows * sizeof(LmPartial));
+    w.part_floats = (size_t)std::max(RES_SPLIT * w.wrows, rows) * d;
+    ALLOC(w.part, w.part_floats * 4);
     ALLOC(w.opart, (size_t)MAX_SPLIT * w.wrows * d * 4);
     ALLOC(w.mlpart, (size_t)MAX_SPLIT * w.wrows * c.n_heads * 2 * 4);
 #undef ALLOC
@@ -321,6 +340,24 @@ struct FwdArgs {
     float* xout;              // residual copy or nullptr
 };
 
+// O / down projection: split-K GEMM into partials, then the reduction that adds
+// them to the residual and prepares the next RMSNorm's operand and partial sums.
+template <int WT, bool XF32>
+int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* gnext, int M, int Mc, int MT, int gy,
+                  hipStream_t s) {
+    Workspace& w = m->ws;
+    const int d = m->cfg.d_model;
+    const int KS = (Mc <= 64 && big(G_RES, W.n_tiles)) ? RES_SPLIT : 1;
+    if ((size_t)KS * Mc * d > w.part_floats) return fail(DLLM_E_INVAL, "internal: split-K buffer too small");
+    GemmArgs g{W.w, W.scale, X, W.KCw, W.KCw * WTraits<WT>::XPER, W.n_tiles, nullptr, 0, 0, 0.f, 0.f};
+    EpiPartial e{w.part, d, Mc};
+    int rc = launch_gemm<WT, G_RES>(W.n_tiles, MT, KS, g, e, gy, s);
+    if (rc) return rc;
+    hipLaunchKernelGGL((residual_reduce_kernel<XF32>), dim3(ceil_div(d, 64), Mc / 4), dim3(256), 0, s,
+                       (const float*)w.part, KS, Mc, d, M, w.x, gnext, w.xg, m->KCx_d, w.ssq, w.rows);
+    return DLLM_OK;
+}
+
 template <int WT, typename AT>   // AT: element type of the embedding and the cache planes
 int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     constexpr bool XF32 = (WT == WT_F32);
@@ -362,9 +399,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
             GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles,
                        w.ssq, n_part, w.rows, 1.0f / d, c.eps};
             EpiQKV<XF32> e{d, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane, kv->Cs};
-            const int F = pick_F(G_QKV, L.qkv.n_tiles, MT);
             ProbeScope ps(m, DLLM_K_QKV, s);
-            if ((rc = launch_gemm<WT, G_QKV>(F, MT, g, e, ceil_div(L.qkv.n_tiles, F), gy, s))) return rc;
+            if ((rc = launch_gemm<WT, G_QKV>(L.qkv.n_tiles, MT, 1, g, e, gy, s))) return rc;
         }
         // attention over [0, T) (+ split merge)
         {
@@ -379,22 +415,22 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 else if (Dh == 64) hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(Mc, H), dim3(64), 0, s, at);
                 else hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(Mc, H), dim3(64), 0, s, at);
             } else {
-                const int QT = (a.M <= 16) ? 1 : 2;
-                const int nqb = ceil_div(Mc, 16 * QT);
+                // one 16-query tile per workgroup (K and V of a block stay in registers);
+                // 8 waves split the key blocks when a head has >= 12 of them, else 4;
+                // key splits across workgroups only for long prefixes
+                const int nqb = Mc / 16;
                 const int nblk = ceil_div(a.T, 32);
+                const int NWA = nblk >= 12 ? 8 : 4;
                 int nsplit = 1;
-                if (a.M <= 64) {
-                    nsplit = std::max(1, std::min(MAX_SPLIT, ceil_div(512, H * nqb)));
-                    nsplit = std::min(nsplit, std::max(1, nblk / 2));
-                }
+                if (a.M <= 64) nsplit = std::max(1, std::min(MAX_SPLIT, nblk / (NWA * 4)));
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
                 dim3 grid(at.nsplit, H, nqb);
-#define ATTN(DH_, QT_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, QT_>), grid, dim3(64), 0, s, at)
+#define ATTN(DH_, NWA_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, 1, NWA_>), grid, dim3(NWA_ * 64), 0, s, at)
                 if (Dh == 128) {
-                    if (QT == 1) ATTN(128, 1); else ATTN(128, 2);
+                    if (NWA == 8) ATTN(128, 8); else ATTN(128, 4);
                 } else {
-                    if (QT == 1) ATTN(64, 1); else ATTN(64, 2);
+                    if (NWA == 8) ATTN(64, 8); else ATTN(64, 4);
                 }
 #undef ATTN
                 if (at.nsplit > 1) {
@@ -408,29 +444,24 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         {
             GemmArgs g{L.o.w, L.o.scale, w.of, L.o.KCw, L.o.KCw * WTraits<WT>::XPER, L.o.n_tiles,
                        nullptr, 0, 0, 0.f, 0.f};
-            EpiResidual<XF32> e{w.x, d, a.M, L.g2, w.xg, m->KCx_d, w.ssq, w.rows};
             ProbeScope ps(m, DLLM_K_OPROJ, s);
-            if ((rc = launch_gemm<WT, G_RES>(1, MT, g, e, L.o.n_tiles, gy, s))) return rc;
-            n_part = L.o.n_tiles;
+            if ((rc = residual_proj<WT, XF32>(m, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) return rc;
+            n_part = ceil_div(d, 64);
         }
         // RMSNorm + gate/up + SwiGLU
         {
             GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles,
                        w.ssq, n_part, w.rows, 1.0f / d, c.eps};
             EpiSwiGLU<XF32> e{w.af, m->KCx_f};
-            const int F = pick_F(G_GU, L.gu.n_tiles, MT);
             ProbeScope ps(m, DLLM_K_GATEUP, s);
-            if ((rc = launch_gemm<WT, G_GU>(F, MT, g, e, ceil_div(L.gu.n_tiles, F), gy, s))) return rc;
+            if ((rc = launch_gemm<WT, G_GU>(L.gu.n_tiles, MT, 1, g, e, gy, s))) return rc;
         }
         // down projection + residual (+ next norm operand)
         {
             const float* gnext = (l + 1 < c.n_layers) ? m->layers[l + 1].g1 : m->gf;
-            GemmArgs g{L.down.w, L.down.scale, w.af, L.down.KCw, L.down.KCw * WTraits<WT>::XPER, L.down.n_tiles,
-                       nullptr, 0, 0, 0.f, 0.f};
-            EpiResidual<XF32> e{w.x, d, a.M, gnext, w.xg, m->KCx_d, w.ssq, w.rows};
             ProbeScope ps(m, DLLM_K_DOWN, s);
-            if ((rc = launch_gemm<WT, G_RES>(1, MT, g, e, L.down.n_tiles, gy, s))) return rc;
-            n_part = L.down.n_tiles;
+            if ((rc = residual_proj<WT, XF32>(m, L.down, w.af, gnext, a.M, Mc, MT, gy, s))) return rc;
+            n_part = ceil_div(d, 64);
         }
     }
     if (a.xout) HIP_TRY(hipMemcpyAsync(a.xout, w.x, (size_t)a.M * d * 4, hipMemcpyDeviceToDevice, s));
@@ -438,12 +469,11 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
         GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles,
                    w.ssq, n_part, w.rows, 1.0f / d, c.eps};
-        const int F = pick_F(G_LM, m->lm.n_tiles, MT);
-        const int gx = ceil_div(m->lm.n_tiles, F);
+        const int gx = row_groups(G_LM, m->lm.n_tiles);
         EpiLM e{c.vocab, c.mask_id, a.M, w.lm, w.wrows, a.logits};
         {
             ProbeScope ps(m, DLLM_K_LMHEAD, s);
-            if ((rc = launch_gemm<WT, G_LM>(F, MT, g, e, gx, gy, s))) return rc;
+            if ((rc = launch_gemm<WT, G_LM>(m->lm.n_tiles, MT, 1, g, e, gy, s))) return rc;
         }
         hipLaunchKernelGGL(lm_combine_kernel, dim3(a.M), dim3(64), 0, s, (const LmPartial*)w.lm, gx, w.wrows,
                            a.out_id, a.out_conf);
@@ -515,8 +545,8 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     m->KCx_d = m->layers[0].qkv.KCw * xper;
     m->KCx_f = m->layers[0].down.KCw * xper;
     (void)xcols;
-    m->n_part_max = std::max(1, m->layers[0].o.n_tiles);
-    m->n_lm_wg = ceil_div(m->lm.n_tiles, std::min(pick_F(G_LM, m->lm.n_tiles, 1), pick_F(G_LM, m->lm.n_tiles, 4)));
+    m->n_part_max = std::max(1, ceil_div(d, 64));
+    m->n_lm_wg = row_groups(G_LM, m->lm.n_tiles);
 
     auto cleanup = [&](int code) {
         dllm_model_destroy(m);

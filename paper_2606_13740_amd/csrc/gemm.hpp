@@ -35,45 +35,52 @@ struct GemmArgs {
     float eps;
 };
 
-// Cooperative per-token 1/RMS from partial sums of squares, computed by one wave.
-// Lane layout: G = mcols/4 float4 groups per partial row, nP = 64/G partial rows
-// in flight per pass; partial sums are combined in LDS in a fixed order.
-__device__ __forceinline__ void rstd_wave(const GemmArgs& g, int m0, int mcols, float* rstd_lds,
-                                          float* tmp_lds /* >= 64 * 4 floats */) {
-    const int lane = threadIdx.x & 63;
-    const int G = mcols >> 2;
-    const int nP = 64 / G;
-    const int grp = lane % G, pr = lane / G;
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-    if (pr < nP) {
-        const float* base = g.ssq + m0 + 4 * grp;
-        int p = pr;
-#pragma unroll 8
-        for (; p < g.n_part; p += nP) {
-            const float4 v = *(const float4*)(base + (size_t)p * g.ssq_ld);
-            s0 += v.x; s1 += v.y; s2 += v.z; s3 += v.w;
+// Per-token 1/RMS of the consumer RMSNorm from partial sums of squares
+// ssq[p][m], p < n_part.  Thread t of the workgroup owns the float4 column group
+// t % G (G = mcols / 4) and the partial rows t / G, t / G + NT / G, ...; its first
+// two loads are issued before the main loop (prefetch) and summed after it; the
+// per-thread sums are combined in LDS in a fixed order.
+template <int NT, int MR>
+struct RstdPrefetch {
+    static constexpr int G = MR / 4;
+    float4 pre[2];
+    __device__ __forceinline__ void issue(const GemmArgs& g, int m0) {
+        const int t = threadIdx.x;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int p = t / G + j * (NT / G);
+            pre[j] = (p < g.n_part) ? *(const float4*)(g.ssq + (size_t)p * g.ssq_ld + m0 + 4 * (t % G))
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        tmp_lds[(pr * G + grp) * 4 + 0] = s0;
-        tmp_lds[(pr * G + grp) * 4 + 1] = s1;
-        tmp_lds[(pr * G + grp) * 4 + 2] = s2;
-        tmp_lds[(pr * G + grp) * 4 + 3] = s3;
     }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (lane < mcols) {
-        const int gg = lane >> 2, c = lane & 3;
-        float t = 0.f;
-        for (int q = 0; q < nP; ++q) t += tmp_lds[(q * G + gg) * 4 + c];
-        rstd_lds[lane] = 1.0f / sqrtf(t * g.inv_d + g.eps);
+    __device__ __forceinline__ void finish(const GemmArgs& g, int m0, float4* tmp /* NT */, float* rstd /* MR */) {
+        const int t = threadIdx.x;
+        float4 s = make_float4(pre[0].x + pre[1].x, pre[0].y + pre[1].y, pre[0].z + pre[1].z, pre[0].w + pre[1].w);
+        for (int p = t / G + 2 * (NT / G); p < g.n_part; p += NT / G) {
+            const float4 v = *(const float4*)(g.ssq + (size_t)p * g.ssq_ld + m0 + 4 * (t % G));
+            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+        tmp[t] = s;
+        __syncthreads();
+        if (t < MR) {
+            const int grp = t >> 2, c = t & 3;
+            float acc = 0.f;
+            for (int q = 0; q < NT / G; ++q) {
+                const float4 v = tmp[q * G + grp];
+                acc += (c == 0) ? v.x : (c == 1) ? v.y : (c == 2) ? v.z : v.w;
+            }
+            rstd[t] = 1.0f / sqrtf(acc * g.inv_d + g.eps);
+        }
+        __syncthreads();
     }
-}
+};
 
-// Epilogue interface:  __device__ void operator()(const float* Y, int ldy, int n0, int nrows,
-//                                                 int m0, int mcols, float* scratch) const
-// Y is LDS [nrows][ldy] holding final outputs (scales and rstd applied); all
-// threads of the workgroup call it; scratch is LDS of at least nrows*ldy floats
-// that the epilogue may overwrite (it aliases Y).
+// Epilogue interface:
+//   __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int part) const
+// Y is LDS [nrows][ldy] holding final outputs of weight rows [n0, n0 + nrows) for
+// tokens [m0, m0 + mcols) (row scales and rstd applied); every thread of the
+// workgroup calls it (it may use __syncthreads and overwrite Y); `part` numbers
+// the row group for per-group partial results.
 
 // Loads in flight per wave: as many K chunks as fit in ~128 VGPRs of buffers.
 template <int WT, int F, int MT>
@@ -84,44 +91,58 @@ constexpr int pipeline_depth() {
     return d < 1 ? 1 : (d > 8 ? 8 : d);
 }
 
-template <int WT, int F, int MT, int NW, bool RSTD, class Epi>
-__global__ void __launch_bounds__((NW + (RSTD ? 1 : 0)) * 64)
+// Workgroup layout: NWn x NWk waves.  Wave (wn, wk) streams FW row tiles (group
+// wn) over slice wk of the workgroup's K range; the NWk slices of a group are
+// summed in LDS in a fixed order.  grid = (row groups / NWn, KS, token blocks):
+// blockIdx.y picks one of KS contiguous K ranges (split-K; the partial results
+// go to an epilogue that stores them for a separate reduction).  With RSTD the
+// consumer RMSNorm's 1/rms per token is reduced from its partial sums as well.
+template <int WT, int FW, int NWn, int NWk, int MT, bool RSTD, class Epi>
+__global__ void __launch_bounds__(NWn * NWk * 64)
 gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int XPER = WTraits<WT>::XPER;
     constexpr bool XF = (WT == WT_F32);
     constexpr int XP = XF ? 1 : 2;                 // activation planes (hi, lo)
     constexpr int XB = XChunk<XF>::bytes;
-    constexpr int D = pipeline_depth<WT, F, MT>();
-    constexpr int NR = 16 * F, MR = 16 * MT, LDY = MR + 1;
-    __shared__ float Y[NR * LDY];
+    constexpr int D = pipeline_depth<WT, FW, MT>();
+    constexpr int NW = NWn * NWk;
+    constexpr int NR = 16 * FW, MR = 16 * MT, LDY = MR + 1;
+    __shared__ float Y[NWn][NR * LDY];
     __shared__ float rstd_lds[64];
-    __shared__ float tmp_lds[64 * 4];
+    __shared__ float4 tmp_lds[RSTD ? NW * 64 : 1];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int nt0 = blockIdx.x * F;
-    const int mt0 = blockIdx.y * MT;
-    const int nf = min(F, g.n_tiles - nt0);  // valid row tiles of this workgroup
+    const int wn = wave % NWn, wk = wave / NWn;
+    const int mt0 = blockIdx.z * MT;
+    const int KS = gridDim.y;
+    const int kb0 = (int)(((long)blockIdx.y * g.KCw) / KS);
+    const int kb1 = (int)(((long)(blockIdx.y + 1) * g.KCw) / KS);
 
-    f32x4_t acc[F][MT];
+    RstdPrefetch<NW * 64, MR> rp;
+    if constexpr (RSTD) rp.issue(g, mt0 * 16);
+
+    f32x4_t acc[FW][MT];
 #pragma unroll
-    for (int f = 0; f < F; ++f)
+    for (int f = 0; f < FW; ++f)
 #pragma unroll
         for (int t = 0; t < MT; ++t) acc[f][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    if (wave < NW) {
-        const int c0 = (int)(((long)wave * g.KCw) / NW);
-        const int c1 = (int)(((long)(wave + 1) * g.KCw) / NW);
+    {
+        const int nt0 = (blockIdx.x * NWn + wn) * FW;
+        const int nf = max(0, min(FW, g.n_tiles - nt0));
+        const int c0 = kb0 + (int)(((long)wk * (kb1 - kb0)) / NWk);
+        const int c1 = kb0 + (int)(((long)(wk + 1) * (kb1 - kb0)) / NWk);
         const char* wp = (const char*)g.W + ((size_t)nt0 * g.KCw * 64 + lane) * 16;
         const char* xp = (const char*)g.X + (size_t)mt0 * g.KCx * XB + lane * 16;
         const size_t wtile = (size_t)g.KCw * 1024, xtile = (size_t)g.KCx * XB;
 
-        u32x4_t wb[D][F];
+        u32x4_t wb[D][FW];
         u32x4_t xb[D][MT * XPER * XP];
 
         auto load = [&](int s, int c) {
 #pragma unroll
-            for (int f = 0; f < F; ++f)
+            for (int f = 0; f < FW; ++f)
                 if (f < nf) wb[s][f] = ldg16_nt(wp + f * wtile + (size_t)c * 1024);
 #pragma unroll
             for (int t = 0; t < MT; ++t)
@@ -134,7 +155,7 @@ gemm_kernel(GemmArgs g, Epi epi) {
         };
         auto compute = [&](int s) {
 #pragma unroll
-            for (int f = 0; f < F; ++f) {
+            for (int f = 0; f < FW; ++f) {
                 if (f >= nf) continue;
                 if constexpr (WT == WT_BF16) {
 #pragma unroll
@@ -163,7 +184,7 @@ gemm_kernel(GemmArgs g, Epi epi) {
             }
         };
 
-        if (c1 > c0) {
+        if (c1 > c0 && nf > 0) {
 #pragma unroll
             for (int s = 0; s < D; ++s) load(s, min(c0 + s, c1 - 1));
             for (int base = c0; base < c1; base += D) {
@@ -176,42 +197,47 @@ gemm_kernel(GemmArgs g, Epi epi) {
                 }
             }
         }
-    } else if constexpr (RSTD) {
-        rstd_wave(g, mt0 * 16, MR, rstd_lds, tmp_lds);
     }
+    if constexpr (RSTD) rp.finish(g, mt0 * 16, tmp_lds, rstd_lds);
 
-    // Combine the NW partial tiles in LDS, wave by wave (fixed order).
+    // Sum the NWk K-slices of each row group into Y[wn], slice by slice (fixed order).
     const int r = lane & 15, gq = lane >> 4;
-    for (int w = 0; w < NW; ++w) {
-        if (wave == w) {
+    for (int k = 0; k < NWk; ++k) {
+        if (wk == k) {
 #pragma unroll
-            for (int f = 0; f < F; ++f)
+            for (int f = 0; f < FW; ++f)
 #pragma unroll
                 for (int t = 0; t < MT; ++t)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        float* p = &Y[(16 * f + 4 * gq + i) * LDY + 16 * t + r];
-                        *p = (w == 0) ? acc[f][t][i] : *p + acc[f][t][i];
+                        float* p = &Y[wn][(16 * f + 4 * gq + i) * LDY + 16 * t + r];
+                        *p = (k == 0) ? acc[f][t][i] : *p + acc[f][t][i];
                     }
         }
         __syncthreads();
     }
 
-    // Row scales and per-token rstd.
-    if (g.wscale != nullptr || RSTD) {
-        for (int idx = threadIdx.x; idx < NR * MR; idx += blockDim.x) {
-            const int n = idx / MR, m = idx % MR;
-            float v = Y[n * LDY + m];
-            if (g.wscale != nullptr) {
-                const int gn = nt0 * 16 + n;
-                v *= (gn < g.n_tiles * 16) ? g.wscale[gn] : 0.f;
+    // Row scales and per-token rstd, then the epilogue of each row group.
+    for (int q = 0; q < NWn; ++q) {
+        const int nt0 = (blockIdx.x * NWn + q) * FW;
+        const int nf = max(0, min(FW, g.n_tiles - nt0));
+        if (nf == 0) break;
+        if (g.wscale != nullptr || RSTD) {
+            for (int idx = threadIdx.x; idx < NR * MR; idx += blockDim.x) {
+                const int n = idx / MR, m = idx % MR;
+                float v = Y[q][n * LDY + m];
+                if (g.wscale != nullptr) {
+                    const int gn = nt0 * 16 + n;
+                    v *= (gn < g.n_tiles * 16) ? g.wscale[gn] : 0.f;
+                }
+                if constexpr (RSTD) v *= rstd_lds[m];
+                Y[q][n * LDY + m] = v;
             }
-            if constexpr (RSTD) v *= rstd_lds[m];
-            Y[n * LDY + m] = v;
+            __syncthreads();
         }
+        epi(Y[q], LDY, nt0 * 16, nf * 16, mt0 * 16, MR, blockIdx.x * NWn + q);
         __syncthreads();
     }
-    epi(Y, LDY, nt0 * 16, nf * 16, mt0 * 16, MR);
 }
 
 // ---------------------------------------------------------------------------
@@ -248,7 +274,7 @@ struct EpiQKV {
         }
     }
 
-    __device__ void operator()(const float* Y, int ldy, int n0, int nrows, int m0, int mcols) const {
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int) const {
         const int npairs = nrows >> 1;
         const int half = Dh >> 1;
         for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
@@ -283,39 +309,17 @@ struct EpiQKV {
     }
 };
 
-// x += Y^T (residual), then the next RMSNorm's A operand xg = bf16(x * g_next)
-// and this workgroup's partial sum of squares of x per token.
-template <bool XF32>
-struct EpiResidual {
-    float* x;               // [rows][d]
-    int d, M;
-    const float* gnext;     // [d]
-    void* xg;               // activation fragments, K = d
-    int KCx;
-    float* ssq;             // [n_part][ssq_ld]
-    int ssq_ld;
+// Split-K partial results: P[ks][m][n] = Y[n][m] (a reduction kernel finishes them).
+struct EpiPartial {
+    float* P;
+    int ldn;                // row length of P (>= packed rows)
+    int rows;               // token rows per K slice of P
 
-    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols) const {
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int) const {
+        float* base = P + (size_t)blockIdx.y * rows * ldn;
         for (int idx = threadIdx.x; idx < nrows * mcols; idx += blockDim.x) {
             const int nl = idx % nrows, ml = idx / nrows;
-            const int m = m0 + ml, n = n0 + nl;
-            float sq = 0.f;
-            if (m < M) {
-                float* xp = x + (size_t)m * d + n;
-                const float xv = *xp + Y[nl * ldy + ml];
-                *xp = xv;
-                xfrag_store<XF32>(xg, m, n, KCx, xv * gnext[n]);
-                sq = xv * xv;
-            } else {
-                xfrag_store<XF32>(xg, m, n, KCx, 0.f);
-            }
-            Y[nl * ldy + ml] = sq;
-        }
-        __syncthreads();
-        for (int ml = threadIdx.x; ml < mcols; ml += blockDim.x) {
-            float s = 0.f;
-            for (int nl = 0; nl < nrows; ++nl) s += Y[nl * ldy + ml];
-            ssq[(size_t)blockIdx.x * ssq_ld + m0 + ml] = s;
+            base[(size_t)(m0 + ml) * ldn + n0 + nl] = Y[nl * ldy + ml];
         }
     }
 };
@@ -327,7 +331,7 @@ struct EpiSwiGLU {
     void* a;
     int KCx;
 
-    __device__ void operator()(const float* Y, int ldy, int n0, int nrows, int m0, int mcols) const {
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int) const {
         const int npairs = nrows >> 1;
         for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
             const int p = idx % npairs, ml = idx / npairs;
@@ -349,11 +353,12 @@ struct LmPartial {
 
 struct EpiLM {
     int V, mask_id, M;
-    LmPartial* part;        // [n_wg][part_ld]
+    LmPartial* part;        // [n_groups][part_ld]
     int part_ld;
     float* logits;          // [M][V] or nullptr
 
-    __device__ void operator()(const float* Y, int ldy, int n0, int nrows, int m0, int mcols) const {
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int grp) const {
+        __shared__ LmPartial red[8][64];
         if (logits != nullptr) {
             for (int idx = threadIdx.x; idx < nrows * mcols; idx += blockDim.x) {
                 const int nl = idx % nrows, ml = idx / nrows;
@@ -362,24 +367,40 @@ struct EpiLM {
                     logits[(size_t)m * V + n] = (n == mask_id) ? -INFINITY : Y[nl * ldy + ml];
             }
         }
-        for (int ml = threadIdx.x; ml < mcols; ml += blockDim.x) {
+        // slice s of the rows for token column ml; 8 slices per column
+        const int per = (nrows + 7) >> 3;
+        for (int idx = threadIdx.x; idx < 8 * mcols; idx += blockDim.x) {
+            const int ml = idx % mcols, sl = idx / mcols;
+            const int b = sl * per, e = min(nrows, b + per);
             float mx = -INFINITY;
             int arg = -1;
-            for (int nl = 0; nl < nrows; ++nl) {
+            for (int nl = b; nl < e; ++nl) {
                 const int n = n0 + nl;
                 if (n >= V || n == mask_id) continue;
                 const float v = Y[nl * ldy + ml];
                 if (v > mx) { mx = v; arg = n; }
             }
             float s = 0.f;
-            if (arg >= 0) {
-                for (int nl = 0; nl < nrows; ++nl) {
+            if (arg >= 0)
+                for (int nl = b; nl < e; ++nl) {
                     const int n = n0 + nl;
                     if (n >= V || n == mask_id) continue;
-                    s += expf(Y[nl * ldy + ml] - mx);
+                    s += __expf(Y[nl * ldy + ml] - mx);
                 }
+            red[sl][ml] = LmPartial{mx, arg, s, 0.f};
+        }
+        __syncthreads();
+        for (int ml = threadIdx.x; ml < mcols; ml += blockDim.x) {
+            LmPartial a = red[0][ml];
+            for (int sl = 1; sl < 8; ++sl) {
+                const LmPartial b = red[sl][ml];
+                if (b.arg < 0) continue;
+                if (a.arg < 0) { a = b; continue; }
+                const float mx = fmaxf(a.mx, b.mx);
+                const int arg = (a.mx > b.mx) ? a.arg : (b.mx > a.mx ? b.arg : min(a.arg, b.arg));
+                a = LmPartial{mx, arg, a.s * __expf(a.mx - mx) + b.s * __expf(b.mx - mx), 0.f};
             }
-            part[(size_t)blockIdx.x * part_ld + m0 + ml] = LmPartial{mx, arg, s, 0.f};
+            part[(size_t)grp * part_ld + m0 + ml] = a;
         }
     }
 };

@@ -41,6 +41,37 @@ embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int
 }
 
 // ---------------------------------------------------------------------------
+// Split-K reduction of a residual projection (O or down):
+//   x[m][n] += sum_ks P[ks][m][n]   (fixed order),
+// then the next RMSNorm's A operand x * g and, per 64-column chunk, the partial
+// sum of squares of x per token.  One wave per token row and column chunk.
+// ---------------------------------------------------------------------------
+template <bool XF32>
+__global__ void __launch_bounds__(256)
+residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float* x, const float* g, void* xg,
+                       int KCx, float* ssq, int ssq_ld) {
+    const int lane = threadIdx.x & 63;
+    const int m = blockIdx.y * 4 + (threadIdx.x >> 6);
+    const int n = blockIdx.x * 64 + lane;
+    float sq = 0.f;
+    if (n < d) {
+        if (m < M) {
+            float acc = 0.f;
+            for (int ks = 0; ks < KS; ++ks) acc += P[((size_t)ks * prow + m) * d + n];
+            float* xp = x + (size_t)m * d + n;
+            const float xv = *xp + acc;
+            *xp = xv;
+            xfrag_store<XF32>(xg, m, n, KCx, xv * g[n]);
+            sq = xv * xv;
+        } else {
+            xfrag_store<XF32>(xg, m, n, KCx, 0.f);
+        }
+    }
+    sq = warp_sum(sq);
+    if (lane == 0) ssq[(size_t)blockIdx.x * ssq_ld + m] = sq;
+}
+
+// ---------------------------------------------------------------------------
 // LM-head merge across vocabulary tiles -> id, confidence = 1 / sum exp(l - max)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ LmPartial lm_merge(LmPartial a, LmPartial b) {
