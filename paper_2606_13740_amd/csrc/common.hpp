@@ -87,6 +87,29 @@ __device__ __forceinline__ void xfrag_store(void* base, int m, int k, int KCx, f
     }
 }
 
+// Store four consecutive activation columns k .. k+3 (k % 4 == 0) of row m.
+template <bool F32>
+__device__ __forceinline__ void xfrag_store4(void* base, int m, int k, int KCx, float4 v) {
+    if (F32) {
+        xfrag_store<true>(base, m, k + 0, KCx, v.x);
+        xfrag_store<true>(base, m, k + 1, KCx, v.y);
+        xfrag_store<true>(base, m, k + 2, KCx, v.z);
+        xfrag_store<true>(base, m, k + 3, KCx, v.w);
+    } else {
+        const int mt = m >> 4, r = m & 15;
+        const int kc = k >> 5, kk = k & 31;
+        const int g = kk >> 3, e = kk & 7;     // e is 0 or 4
+        char* p = (char*)base + (size_t)(mt * KCx + kc) * 2048 + (r + 16 * g) * 16 + e * 2;
+        uint16_t h[4], l[4];
+        split_bf16(v.x, h[0], l[0]);
+        split_bf16(v.y, h[1], l[1]);
+        split_bf16(v.z, h[2], l[2]);
+        split_bf16(v.w, h[3], l[3]);
+        *(uint2*)p = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+        *(uint2*)(p + 1024) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+    }
+}
+
 __device__ __forceinline__ f32x4_t mfma_bf16(const u32x4_t& a, const u32x4_t& b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);

@@ -66,7 +66,6 @@ struct Workspace {
     void* q = nullptr;       // [rows][d] act type
     void* of = nullptr;      // fragments, K = d (attention output)
     void* af = nullptr;      // fragments, K = d_ff
-    float* ssq = nullptr;    // [n_part_max][rows]
     int* pos = nullptr;      // [rows]
     int* lim = nullptr;      // [rows]
     LmPartial* lm = nullptr; // [n_lm_wg][wrows]
@@ -97,7 +96,6 @@ struct dllm_model {
     float* spool = nullptr;  // int8 scales
     float* gpool = nullptr;  // norm gains
     Workspace ws;
-    int n_part_max = 1;
     int n_lm_wg = 1;
     // probe
     int probe_class = -1;
@@ -146,18 +144,18 @@ bool big(GemmKind k, int n_tiles) {
     }
 }
 
-template <int WT, int FW, int NWn, int NWk, int MT, bool RSTD, class Epi>
+template <int WT, int FW, int NWn, int NWk, int MT, class Epi>
 void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
     dim3 grid(ceil_div(n_tiles, FW * NWn), KS, gy);
-    hipLaunchKernelGGL((gemm_kernel<WT, FW, NWn, NWk, MT, RSTD, Epi>), grid, dim3(NWn * NWk * 64), 0, s, g, epi);
+    hipLaunchKernelGGL((gemm_kernel<WT, FW, NWn, NWk, MT, Epi>), grid, dim3(NWn * NWk * 64), 0, s, g, epi);
 }
 
-template <int WT, int FW, int NWn, int NWk, bool RSTD, class Epi>
+template <int WT, int FW, int NWn, int NWk, class Epi>
 int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
     switch (MT) {
-        case 1: launch_gemm_inst<WT, FW, NWn, NWk, 1, RSTD>(g, epi, n_tiles, KS, gy, s); break;
-        case 2: launch_gemm_inst<WT, FW, NWn, NWk, 2, RSTD>(g, epi, n_tiles, KS, gy, s); break;
-        case 4: launch_gemm_inst<WT, FW, NWn, NWk, 4, RSTD>(g, epi, n_tiles, KS, gy, s); break;
+        case 1: launch_gemm_inst<WT, FW, NWn, NWk, 1>(g, epi, n_tiles, KS, gy, s); break;
+        case 2: launch_gemm_inst<WT, FW, NWn, NWk, 2>(g, epi, n_tiles, KS, gy, s); break;
+        case 4: launch_gemm_inst<WT, FW, NWn, NWk, 4>(g, epi, n_tiles, KS, gy, s); break;
         default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
     }
     return DLLM_OK;
@@ -177,17 +175,17 @@ template <int WT, GemmKind KIND, class Epi>
 int launch_gemm(int n_tiles, int MT, int KS, const GemmArgs& g, const Epi& epi, int gy, hipStream_t s) {
     const bool b = big(KIND, n_tiles);
     if constexpr (KIND == G_QKV) {
-        if (b) return launch_gemm_mt<WT, 3, 1, 8, true>(MT, g, epi, n_tiles, 1, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4, true>(MT, g, epi, n_tiles, 1, gy, s);
+        if (b) return launch_gemm_mt<WT, 3, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
     } else if constexpr (KIND == G_GU) {
-        if (b) return launch_gemm_mt<WT, 6, 1, 8, true>(MT, g, epi, n_tiles, 1, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4, true>(MT, g, epi, n_tiles, 1, gy, s);
+        if (b) return launch_gemm_mt<WT, 6, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
     } else if constexpr (KIND == G_LM) {
-        if (b) return launch_gemm_mt<WT, 8, 4, 1, true>(MT, g, epi, n_tiles, 1, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4, true>(MT, g, epi, n_tiles, 1, gy, s);
+        if (b) return launch_gemm_mt<WT, 8, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
     } else {
-        if (b) return launch_gemm_mt<WT, 4, 1, 4, false>(MT, g, epi, n_tiles, KS, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4, false>(MT, g, epi, n_tiles, KS, gy, s);
+        if (b) return launch_gemm_mt<WT, 4, 1, 4>(MT, g, epi, n_tiles, KS, gy, s);
+        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, KS, gy, s);
     }
 }
 
@@ -216,7 +214,7 @@ struct ProbeScope {
 // ---------------------------------------------------------------------------
 
 void free_ws(Workspace& w) {
-    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.ssq, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart};
+    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     w = Workspace{};
@@ -252,7 +250,6 @@ int ensure_ws(dllm_model* m, int rows_needed) {
     ALLOC(w.q, (size_t)rows * d * 4);   // fp32, or bf16 hi and lo planes
     ALLOC(w.of, w.of_bytes);
     ALLOC(w.af, w.af_bytes);
-    ALLOC(w.ssq, (size_t)m->n_part_max * rows * 4);
     ALLOC(w.pos, (size_t)rows * 4);
     ALLOC(w.lim, (size_t)rows * 4);
     ALLOC(w.lm, (size_t)m->n_lm_wg * w.wrows * sizeof(LmPartial));
@@ -316,6 +313,7 @@ int validate_config(const dllm_config* c) {
         return fail(DLLM_E_DTYPE, "bf16 / int8 models need head_dim 64 or 128");
     }
     if (c->d_model % 32 != 0) return fail(DLLM_E_DTYPE, "d_model must be a multiple of 32");
+    if (c->d_model > 4 * ROW_NT * ROW_VPT) return fail(DLLM_E_DTYPE, "d_model must be <= 8192");
     if (c->d_ff % 8 != 0) return fail(DLLM_E_DTYPE, "d_ff must be a multiple of 8");
     return DLLM_OK;
 }
@@ -349,12 +347,12 @@ int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* g
     const int d = m->cfg.d_model;
     const int KS = (Mc <= 64 && big(G_RES, W.n_tiles)) ? RES_SPLIT : 1;
     if ((size_t)KS * Mc * d > w.part_floats) return fail(DLLM_E_INVAL, "internal: split-K buffer too small");
-    GemmArgs g{W.w, W.scale, X, W.KCw, W.KCw * WTraits<WT>::XPER, W.n_tiles, nullptr, 0, 0, 0.f, 0.f};
+    GemmArgs g{W.w, W.scale, X, W.KCw, W.KCw * WTraits<WT>::XPER, W.n_tiles};
     EpiPartial e{w.part, d, Mc};
     int rc = launch_gemm<WT, G_RES>(W.n_tiles, MT, KS, g, e, gy, s);
     if (rc) return rc;
-    hipLaunchKernelGGL((residual_reduce_kernel<XF32>), dim3(ceil_div(d, 64), Mc / 4), dim3(256), 0, s,
-                       (const float*)w.part, KS, Mc, d, M, w.x, gnext, w.xg, m->KCx_d, w.ssq, w.rows);
+    hipLaunchKernelGGL((residual_reduce_kernel<XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const float*)w.part, KS, Mc, d,
+                       M, m->cfg.eps, w.x, gnext, w.xg, m->KCx_d);
     return DLLM_OK;
 }
 
@@ -380,9 +378,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (a.lm && Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
     }
 
-    hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(256), 0, s, (const AT*)m->embed, a.tok, a.mask, a.M,
-                       d, c.vocab, c.mask_id, (const float*)m->layers[0].g1, w.x, w.xg, m->KCx_d, w.ssq);
-    int n_part = 1;
+    hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const AT*)m->embed, a.tok, a.mask,
+                       a.M, d, c.vocab, c.mask_id, c.eps, (const float*)m->layers[0].g1, w.x, w.xg, m->KCx_d);
 
     // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo].
     const size_t plane = (size_t)H * kv->Cs * Dh;
@@ -396,8 +393,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
 
         // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
         {
-            GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles,
-                       w.ssq, n_part, w.rows, 1.0f / d, c.eps};
+            GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles};
             EpiQKV<XF32> e{d, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane, kv->Cs};
             ProbeScope ps(m, DLLM_K_QKV, s);
             if ((rc = launch_gemm<WT, G_QKV>(L.qkv.n_tiles, MT, 1, g, e, gy, s))) return rc;
@@ -440,18 +436,14 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 }
             }
         }
-        // O projection + residual (+ norm-2 operand and partial sums of squares)
+        // O projection + residual (+ the norm-2 operand)
         {
-            GemmArgs g{L.o.w, L.o.scale, w.of, L.o.KCw, L.o.KCw * WTraits<WT>::XPER, L.o.n_tiles,
-                       nullptr, 0, 0, 0.f, 0.f};
             ProbeScope ps(m, DLLM_K_OPROJ, s);
             if ((rc = residual_proj<WT, XF32>(m, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) return rc;
-            n_part = ceil_div(d, 64);
         }
         // RMSNorm + gate/up + SwiGLU
         {
-            GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles,
-                       w.ssq, n_part, w.rows, 1.0f / d, c.eps};
+            GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles};
             EpiSwiGLU<XF32> e{w.af, m->KCx_f};
             ProbeScope ps(m, DLLM_K_GATEUP, s);
             if ((rc = launch_gemm<WT, G_GU>(L.gu.n_tiles, MT, 1, g, e, gy, s))) return rc;
@@ -461,14 +453,12 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
             const float* gnext = (l + 1 < c.n_layers) ? m->layers[l + 1].g1 : m->gf;
             ProbeScope ps(m, DLLM_K_DOWN, s);
             if ((rc = residual_proj<WT, XF32>(m, L.down, w.af, gnext, a.M, Mc, MT, gy, s))) return rc;
-            n_part = ceil_div(d, 64);
         }
     }
     if (a.xout) HIP_TRY(hipMemcpyAsync(a.xout, w.x, (size_t)a.M * d * 4, hipMemcpyDeviceToDevice, s));
     if (a.lm) {
         if (Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
-        GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles,
-                   w.ssq, n_part, w.rows, 1.0f / d, c.eps};
+        GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles};
         const int gx = row_groups(G_LM, m->lm.n_tiles);
         EpiLM e{c.vocab, c.mask_id, a.M, w.lm, w.wrows, a.logits};
         {
@@ -545,7 +535,6 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     m->KCx_d = m->layers[0].qkv.KCw * xper;
     m->KCx_f = m->layers[0].down.KCw * xper;
     (void)xcols;
-    m->n_part_max = std::max(1, ceil_div(d, 64));
     m->n_lm_wg = row_groups(G_LM, m->lm.n_tiles);
 
     auto cleanup = [&](int code) {

@@ -9,9 +9,9 @@
 // The finished tile goes to an epilogue functor that applies the op the
 // projection feeds (RoPE + KV write, residual, SwiGLU, LM-head reduction).
 //
-// Row scales (int8 weights) multiply Y per weight row; the RMSNorm factor
-// rstd[m] of the consumer norm multiplies Y per token column: both factor out of
-// the K sum, so the A operand only carries x * g (rounded once).
+// Row scales (int8 weights) multiply Y per weight row (they factor out of the K
+// sum).  The A operand arrives already normalised (RMSNorm applied by the
+// kernel that finished the residual row).
 #pragma once
 
 #include <type_traits>
@@ -27,58 +27,12 @@ struct GemmArgs {
     int KCw;              // weight chunks per row tile
     int KCx;              // activation chunks per token tile
     int n_tiles;          // packed rows / 16
-    // RMSNorm of the consumer: rstd[m] = 1 / sqrt(sum_p ssq[p][m] / d + eps)
-    const float* ssq;     // [n_part][ssq_ld] partial sums of squares, or nullptr
-    int n_part;
-    int ssq_ld;
-    float inv_d;
-    float eps;
-};
-
-// Per-token 1/RMS of the consumer RMSNorm from partial sums of squares
-// ssq[p][m], p < n_part.  Thread t of the workgroup owns the float4 column group
-// t % G (G = mcols / 4) and the partial rows t / G, t / G + NT / G, ...; its first
-// two loads are issued before the main loop (prefetch) and summed after it; the
-// per-thread sums are combined in LDS in a fixed order.
-template <int NT, int MR>
-struct RstdPrefetch {
-    static constexpr int G = MR / 4;
-    float4 pre[2];
-    __device__ __forceinline__ void issue(const GemmArgs& g, int m0) {
-        const int t = threadIdx.x;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int p = t / G + j * (NT / G);
-            pre[j] = (p < g.n_part) ? *(const float4*)(g.ssq + (size_t)p * g.ssq_ld + m0 + 4 * (t % G))
-                                    : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-    }
-    __device__ __forceinline__ void finish(const GemmArgs& g, int m0, float4* tmp /* NT */, float* rstd /* MR */) {
-        const int t = threadIdx.x;
-        float4 s = make_float4(pre[0].x + pre[1].x, pre[0].y + pre[1].y, pre[0].z + pre[1].z, pre[0].w + pre[1].w);
-        for (int p = t / G + 2 * (NT / G); p < g.n_part; p += NT / G) {
-            const float4 v = *(const float4*)(g.ssq + (size_t)p * g.ssq_ld + m0 + 4 * (t % G));
-            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-        }
-        tmp[t] = s;
-        __syncthreads();
-        if (t < MR) {
-            const int grp = t >> 2, c = t & 3;
-            float acc = 0.f;
-            for (int q = 0; q < NT / G; ++q) {
-                const float4 v = tmp[q * G + grp];
-                acc += (c == 0) ? v.x : (c == 1) ? v.y : (c == 2) ? v.z : v.w;
-            }
-            rstd[t] = 1.0f / sqrtf(acc * g.inv_d + g.eps);
-        }
-        __syncthreads();
-    }
 };
 
 // Epilogue interface:
 //   __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int part) const
 // Y is LDS [nrows][ldy] holding final outputs of weight rows [n0, n0 + nrows) for
-// tokens [m0, m0 + mcols) (row scales and rstd applied); every thread of the
+// tokens [m0, m0 + mcols) (int8 row scales applied); every thread of the
 // workgroup calls it (it may use __syncthreads and overwrite Y); `part` numbers
 // the row group for per-group partial results.
 
@@ -95,9 +49,8 @@ constexpr int pipeline_depth() {
 // wn) over slice wk of the workgroup's K range; the NWk slices of a group are
 // summed in LDS in a fixed order.  grid = (row groups / NWn, KS, token blocks):
 // blockIdx.y picks one of KS contiguous K ranges (split-K; the partial results
-// go to an epilogue that stores them for a separate reduction).  With RSTD the
-// consumer RMSNorm's 1/rms per token is reduced from its partial sums as well.
-template <int WT, int FW, int NWn, int NWk, int MT, bool RSTD, class Epi>
+// go to an epilogue that stores them for a separate reduction).
+template <int WT, int FW, int NWn, int NWk, int MT, class Epi>
 __global__ void __launch_bounds__(NWn * NWk * 64)
 gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int XPER = WTraits<WT>::XPER;
@@ -108,8 +61,6 @@ gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int NW = NWn * NWk;
     constexpr int NR = 16 * FW, MR = 16 * MT, LDY = MR + 1;
     __shared__ float Y[NWn][NR * LDY];
-    __shared__ float rstd_lds[64];
-    __shared__ float4 tmp_lds[RSTD ? NW * 64 : 1];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -118,9 +69,6 @@ gemm_kernel(GemmArgs g, Epi epi) {
     const int KS = gridDim.y;
     const int kb0 = (int)(((long)blockIdx.y * g.KCw) / KS);
     const int kb1 = (int)(((long)(blockIdx.y + 1) * g.KCw) / KS);
-
-    RstdPrefetch<NW * 64, MR> rp;
-    if constexpr (RSTD) rp.issue(g, mt0 * 16);
 
     f32x4_t acc[FW][MT];
 #pragma unroll
@@ -198,7 +146,6 @@ gemm_kernel(GemmArgs g, Epi epi) {
             }
         }
     }
-    if constexpr (RSTD) rp.finish(g, mt0 * 16, tmp_lds, rstd_lds);
 
     // Sum the NWk K-slices of each row group into Y[wn], slice by slice (fixed order).
     const int r = lane & 15, gq = lane >> 4;
@@ -217,21 +164,15 @@ gemm_kernel(GemmArgs g, Epi epi) {
         __syncthreads();
     }
 
-    // Row scales and per-token rstd, then the epilogue of each row group.
+    // Row scales (int8), then the epilogue of each row group.
     for (int q = 0; q < NWn; ++q) {
         const int nt0 = (blockIdx.x * NWn + q) * FW;
         const int nf = max(0, min(FW, g.n_tiles - nt0));
         if (nf == 0) break;
-        if (g.wscale != nullptr || RSTD) {
+        if (g.wscale != nullptr) {
             for (int idx = threadIdx.x; idx < NR * MR; idx += blockDim.x) {
                 const int n = idx / MR, m = idx % MR;
-                float v = Y[q][n * LDY + m];
-                if (g.wscale != nullptr) {
-                    const int gn = nt0 * 16 + n;
-                    v *= (gn < g.n_tiles * 16) ? g.wscale[gn] : 0.f;
-                }
-                if constexpr (RSTD) v *= rstd_lds[m];
-                Y[q][n * LDY + m] = v;
+                Y[q][n * LDY + m] *= g.wscale[nt0 * 16 + n];
             }
             __syncthreads();
         }

@@ -8,67 +8,101 @@
 namespace dllm {
 
 // ---------------------------------------------------------------------------
-// Embedding gather: x[m] = E[id_m] (the MASK id where the mask flag is set), the
-// first RMSNorm's A operand x * g, and sum(x^2) as the single norm partial.
+// Row-wise RMSNorm operand: given the finished residual row x[m][0..d), write
+// the next GEMM's A operand h = x * rsqrt(mean(x^2) + eps) * g into the
+// activation fragments.  Each thread holds VPT column groups of 4 values.
 // ---------------------------------------------------------------------------
-template <typename ET, bool XF32>
-__global__ void __launch_bounds__(256)
-embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int V, int mask_id,
-             const float* g, float* x, void* xg, int KCx, float* ssq) {
-    __shared__ float red[4];
-    const int m = blockIdx.x;
-    float sq = 0.f;
-    if (m < M) {
-        int id = (mask != nullptr && mask[m]) ? mask_id : tok[m];
-        if (id < 0 || id >= V) id = mask_id;
-        const ET* row = E + (size_t)id * d;
-        for (int n = threadIdx.x; n < d; n += blockDim.x) {
-            const float v = to_f32<ET>(row[n]);
-            x[(size_t)m * d + n] = v;
-            xfrag_store<XF32>(xg, m, n, KCx, v * g[n]);
-            sq += v * v;
-        }
-    } else {
-        for (int n = threadIdx.x; n < d; n += blockDim.x) {
-            x[(size_t)m * d + n] = 0.f;
-            xfrag_store<XF32>(xg, m, n, KCx, 0.f);
-        }
-    }
-    sq = warp_sum(sq);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* red /* NT/64 */) {
+    v = warp_sum(v);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
     __syncthreads();
-    if (threadIdx.x == 0) ssq[m] = red[0] + red[1] + red[2] + red[3];
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) s += red[w];
+    __syncthreads();
+    return s;
 }
 
-// ---------------------------------------------------------------------------
-// Split-K reduction of a residual projection (O or down):
-//   x[m][n] += sum_ks P[ks][m][n]   (fixed order),
-// then the next RMSNorm's A operand x * g and, per 64-column chunk, the partial
-// sum of squares of x per token.  One wave per token row and column chunk.
-// ---------------------------------------------------------------------------
-template <bool XF32>
-__global__ void __launch_bounds__(256)
-residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float* x, const float* g, void* xg,
-                       int KCx, float* ssq, int ssq_ld) {
-    const int lane = threadIdx.x & 63;
-    const int m = blockIdx.y * 4 + (threadIdx.x >> 6);
-    const int n = blockIdx.x * 64 + lane;
+template <bool XF32, int NT, int VPT>
+__device__ __forceinline__ void write_norm_operand(const float4 (&xv)[VPT], int m, int d, float eps, const float* g,
+                                                   void* xg, int KCx, float* red) {
     float sq = 0.f;
-    if (n < d) {
-        if (m < M) {
-            float acc = 0.f;
-            for (int ks = 0; ks < KS; ++ks) acc += P[((size_t)ks * prow + m) * d + n];
-            float* xp = x + (size_t)m * d + n;
-            const float xv = *xp + acc;
-            *xp = xv;
-            xfrag_store<XF32>(xg, m, n, KCx, xv * g[n]);
-            sq = xv * xv;
-        } else {
-            xfrag_store<XF32>(xg, m, n, KCx, 0.f);
-        }
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+        const int n = 4 * (threadIdx.x + j * NT);
+        if (n < d) sq += xv[j].x * xv[j].x + xv[j].y * xv[j].y + xv[j].z * xv[j].z + xv[j].w * xv[j].w;
     }
-    sq = warp_sum(sq);
-    if (lane == 0) ssq[(size_t)blockIdx.x * ssq_ld + m] = sq;
+    const float rs = 1.0f / sqrtf(block_sum<NT>(sq, red) / d + eps);
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+        const int n = 4 * (threadIdx.x + j * NT);
+        if (n >= d) continue;
+        const float4 gg = *(const float4*)(g + n);
+        xfrag_store4<XF32>(xg, m, n, KCx,
+                           make_float4(xv[j].x * rs * gg.x, xv[j].y * rs * gg.y, xv[j].z * rs * gg.z,
+                                       xv[j].w * rs * gg.w));
+    }
+}
+
+// Rows of the residual kernels: NT threads x VPT float4 groups cover d <= 4*NT*VPT.
+constexpr int ROW_NT = 1024;
+constexpr int ROW_VPT = 2;      // d up to 8192
+
+// Embedding gather: x[m] = E[id_m] (the MASK id where the mask flag is set) and
+// the first layer's normalised operand.  Padding rows get zeros.
+template <typename ET, bool XF32>
+__global__ void __launch_bounds__(ROW_NT)
+embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int V, int mask_id, float eps,
+             const float* g, float* x, void* xg, int KCx) {
+    __shared__ float red[ROW_NT / 64];
+    const int m = blockIdx.x;
+    float4 xv[ROW_VPT];
+    int id = -1;
+    if (m < M) {
+        id = (mask != nullptr && mask[m]) ? mask_id : tok[m];
+        if (id < 0 || id >= V) id = mask_id;
+    }
+#pragma unroll
+    for (int j = 0; j < ROW_VPT; ++j) {
+        const int n = 4 * (threadIdx.x + j * ROW_NT);
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (n < d && id >= 0) {
+            const ET* row = E + (size_t)id * d + n;
+            v = make_float4(to_f32<ET>(row[0]), to_f32<ET>(row[1]), to_f32<ET>(row[2]), to_f32<ET>(row[3]));
+        }
+        xv[j] = v;
+        if (n < d) *(float4*)(x + (size_t)m * d + n) = v;
+    }
+    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red);
+}
+
+// Split-K reduction of a residual projection (O or down), one workgroup per row:
+//   x[m][n] += sum_ks P[ks][m][n]   (fixed order),
+// then the next RMSNorm's normalised operand.  Padding rows get zeros.
+template <bool XF32>
+__global__ void __launch_bounds__(ROW_NT)
+residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps, float* x, const float* g,
+                       void* xg, int KCx) {
+    __shared__ float red[ROW_NT / 64];
+    const int m = blockIdx.x;
+    float4 xv[ROW_VPT];
+#pragma unroll
+    for (int j = 0; j < ROW_VPT; ++j) {
+        const int n = 4 * (threadIdx.x + j * ROW_NT);
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (n < d && m < M) {
+            float4* xp = (float4*)(x + (size_t)m * d + n);
+            v = *xp;
+            for (int ks = 0; ks < KS; ++ks) {
+                const float4 p = *(const float4*)(P + ((size_t)ks * prow + m) * d + n);
+                v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+            }
+            *xp = v;
+        }
+        xv[j] = v;
+    }
+    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red);
 }
 
 // ---------------------------------------------------------------------------
