@@ -42,26 +42,36 @@ struct AttnArgs {
 // product takes three MFMAs (hi*hi + hi*lo + lo*hi), so scores and outputs keep
 // ~16 significant bits; the probabilities P are split the same way.
 //
-// Workgroup = (split, head, query block of 16*QT rows) with NWA waves; the
-// split's 32-key blocks are dealt out to the waves in contiguous runs, each
-// wave keeps its own online softmax, and the waves are merged in LDS (max over
-// waves, then the rescaled outputs summed wave by wave in a fixed order).  With
-// one split the normalised output goes straight to the O projection's
-// fragments; otherwise (m, l, o) per split goes to attn_combine.
-template <int DH, int QT, int NWA>
-__global__ void __launch_bounds__(NWA * 64) attn_bf16_kernel(AttnArgs a) {
-    constexpr int NC = DH / 32;     // 32-dim chunks
-    constexpr int ND = DH / 16;     // 16-dim output tiles
-    constexpr int NQ = 16 * QT;     // query rows of the workgroup
-    __shared__ float mx_s[NWA][NQ];
-    __shared__ float l_s[NWA][NQ];
-    __shared__ float obuf[NQ][DH + 1];
-    __shared__ float Mq[NQ], Lq[NQ];
+// Workgroup = (key split, head, group of QG query tiles of 16 rows), one wave per
+// query tile.  The split's 32-key blocks are staged in LDS once per workgroup
+// with direct global->LDS loads (global_load_lds_dwordx4), double-buffered so the
+// next block streams in while the current one is used, and every wave reads its
+// MFMA fragments from LDS.  LDS rows are XOR-swizzled in 16-byte columns so that
+// the 16 rows one fragment read touches fall in distinct banks:
+//   K plane  [32 keys][Dh/8 cols]: col' = col ^ (((key & 3) | (4 * ((key >> 3) & 3))) mod Dh/8)
+//   V^T plane [Dh dims][4 cols]:   col' = col ^ ((dim >> 2) & 3)
+// With one split the normalised output goes to the O projection's fragments;
+// otherwise (m, l, o) per split goes to attn_combine.
+__device__ __forceinline__ int swz_k(int key) { return (key & 3) | (((key >> 3) & 3) << 2); }
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int DH, int QG>
+__global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
+    constexpr int NC = DH / 32;               // 32-dim chunks
+    constexpr int ND = DH / 16;               // 16-dim output tiles
+    constexpr int KCOLS = DH / 8;             // 16-byte columns per key row
+    constexpr int KPLANE = 32 * DH * 2;       // bytes of one K plane of a block
+    constexpr int VPLANE = DH * 64;           // bytes of one V^T plane of a block
+    constexpr int BUF = 2 * KPLANE + 2 * VPLANE;
+    constexpr int NSLOT = BUF / 16;           // 16-byte slots per block
+    static_assert(NSLOT % 64 == 0, "block must be whole wave loads");
+    __shared__ __attribute__((aligned(1024))) char lds[2 * BUF];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, h = blockIdx.y;
-    const int row0 = blockIdx.z * NQ;
+    const int row = blockIdx.z * 16 * QG + 16 * wave + r;    // this lane's query row
     const int ld = a.H * DH;
     const float sl2 = a.scale * 1.4426950408889634f;
 
@@ -70,189 +80,150 @@ __global__ void __launch_bounds__(NWA * 64) attn_bf16_kernel(AttnArgs a) {
     const uint16_t* Vp = (const uint16_t*)a.Vt + (size_t)h * DH * a.Cs;
 
     const int nblk = (a.T + 31) >> 5;
-    const int sb0 = split * a.bps, sb1 = min(nblk, sb0 + a.bps);
-    const int kb0 = sb0 + (int)(((long)wave * (sb1 - sb0)) / NWA);
-    const int kb1 = sb0 + (int)(((long)(wave + 1) * (sb1 - sb0)) / NWA);
+    const int kb0 = split * a.bps, kb1 = min(nblk, kb0 + a.bps);
 
-    u32x4_t qf[QT][NC][2];
-    int lim[QT];
+    // stage block kb into buffer `buf`: slot s -> K plane / V^T plane position
+    auto stage = [&](int kb, int buf) {
+        const int k0 = kb * 32;
+        char* base = lds + buf * BUF;
 #pragma unroll
-    for (int t = 0; t < QT; ++t) {
-        const int row = row0 + 16 * t + r;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const uint16_t* src = qp + (size_t)row * ld + h * DH + 32 * c + 8 * g;
-            qf[t][c][0] = ldg16(src);
-            qf[t][c][1] = ldg16(src + a.q_plane);
+        for (int i = wave; i < NSLOT / 64; i += QG) {
+            const int sl = i * 64 + lane;
+            const uint16_t* src;
+            if (sl < KPLANE / 8) {                       // K: two planes of 32 x KCOLS slots
+                const int pl = sl / (KPLANE / 16), s2 = sl % (KPLANE / 16);
+                const int key = s2 / KCOLS, pc = s2 % KCOLS;
+                const int col = pc ^ (swz_k(key) & (KCOLS - 1));
+                src = Kp + pl * a.kv_plane + (size_t)(k0 + key) * DH + col * 8;
+            } else {                                     // V^T: two planes of DH x 4 slots
+                const int s1 = sl - KPLANE / 8;
+                const int pl = s1 / (VPLANE / 16), s2 = s1 % (VPLANE / 16);
+                const int dim = s2 >> 2, pc = s2 & 3;
+                const int col = pc ^ ((dim >> 2) & 3);
+                src = Vp + pl * a.kv_plane + (size_t)dim * a.Cs + k0 + col * 8;
+            }
+            __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(base + i * 1024), 16, 0, 0);
         }
-        lim[t] = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
-    }
+    };
 
-    float mrun[QT], lrun[QT];
-    f32x4_t oacc[ND][QT];
-#pragma unroll
-    for (int t = 0; t < QT; ++t) {
-        mrun[t] = -INFINITY;
-        lrun[t] = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) oacc[dt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
+    if (kb0 < kb1) stage(kb0, 0);
 
-    const int krow0 = 8 * (r >> 2) + (r & 3);   // + 4t: the key this lane loads for tile t
+    u32x4_t qf[NC][2];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const uint16_t* src = qp + (size_t)row * ld + h * DH + 32 * c + 8 * g;
+        qf[c][0] = ldg16(src);
+        qf[c][1] = ldg16(src + a.q_plane);
+    }
+    const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
+
+    float mrun = -INFINITY, lrun = 0.f;
+    f32x4_t oacc[ND];
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int krow0 = 8 * (r >> 2) + (r & 3);   // + 4t: the key this lane reads for tile t
 
     for (int kb = kb0; kb < kb1; ++kb) {
+        const int cur = (kb - kb0) & 1;
+        __builtin_amdgcn_s_waitcnt(0);          // this wave's loads into `cur` have landed
+        __syncthreads();                        // ... and everyone's; `cur ^ 1` is free again
+        if (kb + 1 < kb1) stage(kb + 1, cur ^ 1);
+        const char* Kb = lds + cur * BUF;
+        const char* Vb = Kb + 2 * KPLANE;
         const int k0 = kb * 32;
-        // issue the block's K and V loads together
-        u32x4_t kf[NC][2][2];
+
+        f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
+        for (int c = 0; c < NC; ++c) {
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                const uint16_t* src = Kp + (size_t)(k0 + krow0 + 4 * t) * DH + 32 * c + 8 * g;
-                kf[c][t][0] = ldg16(src);
-                kf[c][t][1] = ldg16(src + a.kv_plane);
+                const int key = krow0 + 4 * t;
+                const int off = key * (DH * 2) + (((4 * c + g) ^ (swz_k(key) & (KCOLS - 1))) << 4);
+                const u32x4_t kh = *(const u32x4_t*)(Kb + off);
+                const u32x4_t kl = *(const u32x4_t*)(Kb + KPLANE + off);
+                f32x4_t& sa = t ? s1 : s0;
+                sa = mfma_bf16(kh, qf[c][0], sa);
+                sa = mfma_bf16(kh, qf[c][1], sa);
+                sa = mfma_bf16(kl, qf[c][0], sa);
             }
-        u32x4_t vf[ND][2];
+        }
+
+        float sv[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int key0 = k0 + 8 * g + i, key1 = key0 + 4;
+            sv[i] = (key0 < lim) ? s0[i] * sl2 : -INFINITY;
+            sv[4 + i] = (key1 < lim) ? s1[i] * sl2 : -INFINITY;
+        }
+        float bm = sv[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) bm = fmaxf(bm, sv[j]);
+        bm = fmaxf(bm, __shfl_xor(bm, 16));
+        bm = fmaxf(bm, __shfl_xor(bm, 32));
+        const float mnew = fmaxf(mrun, bm);
+        float alpha = 1.f, ps = 0.f;
+        uint32_t phi[4] = {0u, 0u, 0u, 0u}, plo[4] = {0u, 0u, 0u, 0u};
+        if (mnew != -INFINITY) {
+            alpha = exp2f(mrun - mnew);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float p0 = exp2f(sv[2 * e] - mnew), p1 = exp2f(sv[2 * e + 1] - mnew);
+                ps += p0 + p1;
+                // p in [0, 1]: hi = truncation, lo = the rounded remainder
+                const uint32_t u0 = __float_as_uint(p0), u1 = __float_as_uint(p1);
+                const float r0 = p0 - __uint_as_float(u0 & 0xFFFF0000u);
+                const float r1 = p1 - __uint_as_float(u1 & 0xFFFF0000u);
+                phi[e] = (u0 >> 16) | (u1 & 0xFFFF0000u);
+                plo[e] = (uint32_t)f32_to_bf16(r0) | ((uint32_t)f32_to_bf16(r1) << 16);
+            }
+        }
+        lrun = lrun * alpha + ps;
+        mrun = mnew;
+        const u32x4_t ph = {phi[0], phi[1], phi[2], phi[3]};
+        const u32x4_t pl = {plo[0], plo[1], plo[2], plo[3]};
+        const bool tail = (k0 + 8 * g + 8 > a.T);
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
-            const uint16_t* src = Vp + (size_t)(16 * dt + r) * a.Cs + k0 + 8 * g;
-            vf[dt][0] = ldg16(src);
-            vf[dt][1] = ldg16(src + a.kv_plane);
-        }
-
-        // scores S^T for both 16-key tiles and every query tile
-        f32x4_t sacc[2][QT];
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int u = 0; u < QT; ++u) sacc[t][u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int u = 0; u < QT; ++u) {
-                    sacc[t][u] = mfma_bf16(kf[c][t][0], qf[u][c][0], sacc[t][u]);
-                    sacc[t][u] = mfma_bf16(kf[c][t][0], qf[u][c][1], sacc[t][u]);
-                    sacc[t][u] = mfma_bf16(kf[c][t][1], qf[u][c][0], sacc[t][u]);
-                }
-
-        u32x4_t pf[QT][2];
-#pragma unroll
-        for (int u = 0; u < QT; ++u) {
-            float sv[8];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key0 = k0 + 8 * g + i, key1 = key0 + 4;
-                sv[i] = (key0 < lim[u]) ? sacc[0][u][i] * sl2 : -INFINITY;
-                sv[4 + i] = (key1 < lim[u]) ? sacc[1][u][i] * sl2 : -INFINITY;
-            }
-            float bm = sv[0];
-#pragma unroll
-            for (int j = 1; j < 8; ++j) bm = fmaxf(bm, sv[j]);
-            bm = fmaxf(bm, __shfl_xor(bm, 16));
-            bm = fmaxf(bm, __shfl_xor(bm, 32));
-            const float mnew = fmaxf(mrun[u], bm);
-            float alpha = 1.f, ps = 0.f;
-            uint32_t phi[4] = {0u, 0u, 0u, 0u}, plo[4] = {0u, 0u, 0u, 0u};
-            if (mnew != -INFINITY) {
-                alpha = exp2f(mrun[u] - mnew);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float p0 = exp2f(sv[2 * e] - mnew), p1 = exp2f(sv[2 * e + 1] - mnew);
-                    ps += p0 + p1;
-                    uint16_t h0, l0, h1, l1;
-                    split_bf16(p0, h0, l0);
-                    split_bf16(p1, h1, l1);
-                    phi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-                    plo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-                }
-            }
-            lrun[u] = lrun[u] * alpha + ps;
-            mrun[u] = mnew;
-            pf[u][0] = u32x4_t{phi[0], phi[1], phi[2], phi[3]};
-            pf[u][1] = u32x4_t{plo[0], plo[1], plo[2], plo[3]};
-#pragma unroll
-            for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) oacc[dt][u][i] *= alpha;
-        }
-
-        // O^T += V^T * P^T
-        if (k0 + 8 * g + 8 > a.T) {            // tail: zero V beyond T (those rows may be unwritten)
-#pragma unroll
-            for (int dt = 0; dt < ND; ++dt)
+            for (int i = 0; i < 4; ++i) oacc[dt][i] *= alpha;
+            const int dim = 16 * dt + r;
+            const int off = dim * 64 + ((g ^ ((dim >> 2) & 3)) << 4);
+            u32x4_t vh = *(const u32x4_t*)(Vb + off);
+            u32x4_t vl = *(const u32x4_t*)(Vb + VPLANE + off);
+            if (tail) {                          // zero V beyond T (those rows may be unwritten)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int key = k0 + 8 * g + 2 * e;
                     const uint32_t keep = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
-                    vf[dt][0][e] &= keep;
-                    vf[dt][1][e] &= keep;
+                    vh[e] &= keep;
+                    vl[e] &= keep;
                 }
+            }
+            oacc[dt] = mfma_bf16(vh, ph, oacc[dt]);
+            oacc[dt] = mfma_bf16(vh, pl, oacc[dt]);
+            oacc[dt] = mfma_bf16(vl, ph, oacc[dt]);
         }
+    }
+
+    float l = lrun;
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    if (a.nsplit == 1) {
+        const float inv = 1.f / l;
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-            for (int u = 0; u < QT; ++u) {
-                oacc[dt][u] = mfma_bf16(vf[dt][0], pf[u][0], oacc[dt][u]);
-                oacc[dt][u] = mfma_bf16(vf[dt][0], pf[u][1], oacc[dt][u]);
-                oacc[dt][u] = mfma_bf16(vf[dt][1], pf[u][0], oacc[dt][u]);
-            }
-    }
-
-    // ---- merge the NWA waves ----
-#pragma unroll
-    for (int u = 0; u < QT; ++u) {
-        float l = lrun[u];
-        l += __shfl_xor(l, 16);
-        l += __shfl_xor(l, 32);
-        if (g == 0) {
-            mx_s[wave][16 * u + r] = mrun[u];
-            l_s[wave][16 * u + r] = l;
-        }
-    }
-    __syncthreads();
-    for (int q = threadIdx.x; q < NQ; q += blockDim.x) {
-        float M = -INFINITY;
-        for (int w = 0; w < NWA; ++w) M = fmaxf(M, mx_s[w][q]);
-        float L = 0.f;
-        for (int w = 0; w < NWA; ++w)
-            if (mx_s[w][q] != -INFINITY) L += l_s[w][q] * exp2f(mx_s[w][q] - M);
-        Mq[q] = M;
-        Lq[q] = L;
-    }
-    __syncthreads();
-    for (int w = 0; w < NWA; ++w) {
-        if (wave == w) {
-#pragma unroll
-            for (int u = 0; u < QT; ++u) {
-                const int q = 16 * u + r;
-                const float sc = (mrun[u] == -INFINITY) ? 0.f : exp2f(mrun[u] - Mq[q]);
-#pragma unroll
-                for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        float* o = &obuf[q][16 * dt + 4 * g + i];
-                        *o = (w == 0 ? 0.f : *o) + oacc[dt][u][i] * sc;
-                    }
-            }
-        }
-        __syncthreads();
-    }
-    if (a.nsplit == 1) {
-        for (int idx = threadIdx.x; idx < NQ * DH; idx += blockDim.x) {
-            const int q = idx / DH, dim = idx % DH;
-            xfrag_store<false>(a.o, row0 + q, h * DH + dim, a.KCx, obuf[q][dim] / Lq[q]);
-        }
+            for (int i = 0; i < 4; ++i)
+                xfrag_store<false>(a.o, row, h * DH + 16 * dt + 4 * g + i, a.KCx, oacc[dt][i] * inv);
     } else {
-        for (int idx = threadIdx.x; idx < NQ * DH; idx += blockDim.x) {
-            const int q = idx / DH, dim = idx % DH;
-            a.opart[(((size_t)split * a.rows_ld + row0 + q) * a.H + h) * DH + dim] = obuf[q][dim];
-        }
-        for (int q = threadIdx.x; q < NQ; q += blockDim.x) {
-            float* ml = a.mlpart + (((size_t)split * a.rows_ld + row0 + q) * a.H + h) * 2;
-            ml[0] = Mq[q];
-            ml[1] = Lq[q];
+        float* op = a.opart + (((size_t)split * a.rows_ld + row) * a.H + h) * DH;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+            *(float4*)(op + 16 * dt + 4 * g) = make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
+        if (g == 0) {
+            float* ml = a.mlpart + (((size_t)split * a.rows_ld + row) * a.H + h) * 2;
+            ml[0] = mrun;
+            ml[1] = l;
         }
     }
 }

@@ -411,23 +411,23 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 else if (Dh == 64) hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(Mc, H), dim3(64), 0, s, at);
                 else hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(Mc, H), dim3(64), 0, s, at);
             } else {
-                // one 16-query tile per workgroup (K and V of a block stay in registers);
-                // 8 waves split the key blocks when a head has >= 12 of them, else 4;
-                // key splits across workgroups only for long prefixes
-                const int nqb = Mc / 16;
+                // QG query tiles share each staged K/V block; key splits across
+                // workgroups give the chip enough waves (~2 per SIMD) and are merged
+                // by attn_combine
+                const int QG = (Mc >= 64) ? 4 : Mc / 16;
+                const int nqg = Mc / (16 * QG);
                 const int nblk = ceil_div(a.T, 32);
-                const int NWA = nblk >= 12 ? 8 : 4;
-                int nsplit = 1;
-                if (a.M <= 64) nsplit = std::max(1, std::min(MAX_SPLIT, nblk / (NWA * 4)));
+                int nsplit = std::max(1, std::min(nblk, 2048 / (H * nqg * QG)));
+                if (a.M > 64) nsplit = std::min(nsplit, 1);          // prefill: enough workgroups already
+                nsplit = std::min(nsplit, MAX_SPLIT);
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
-                dim3 grid(at.nsplit, H, nqb);
-#define ATTN(DH_, NWA_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, 1, NWA_>), grid, dim3(NWA_ * 64), 0, s, at)
-                if (Dh == 128) {
-                    if (NWA == 8) ATTN(128, 8); else ATTN(128, 4);
-                } else {
-                    if (NWA == 8) ATTN(64, 8); else ATTN(64, 4);
-                }
+                dim3 grid(at.nsplit, H, nqg);
+#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, QG_>), grid, dim3(QG_ * 64), 0, s, at)
+#define ATTN_QG(DH_) \
+    do { if (QG == 4) ATTN(DH_, 4); else if (QG == 2) ATTN(DH_, 2); else ATTN(DH_, 1); } while (0)
+                if (Dh == 128) ATTN_QG(128); else ATTN_QG(64);
+#undef ATTN_QG
 #undef ATTN
                 if (at.nsplit > 1) {
                     const int total = Mc * H * Dh;
