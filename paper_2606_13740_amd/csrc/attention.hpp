@@ -229,26 +229,33 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
 }
 
 // Merge key-range splits: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M).
+// 32 lanes per (row, head), four consecutive dims per lane; 8 (row, head) pairs
+// per 256-thread workgroup.
 template <bool XF32>
 __global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a, int rows, int DH) {
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    const int total = rows * a.H * DH;
-    if (idx >= total) return;
-    const int dim = idx % DH;
-    const int h = (idx / DH) % a.H;
-    const int row = idx / (DH * a.H);
+    const int pair = blockIdx.x * 8 + (threadIdx.x >> 5);
+    const int l = threadIdx.x & 31;
+    if (pair >= rows * a.H) return;
+    const int h = pair % a.H, row = pair / a.H;
+    const size_t stride_s = (size_t)a.rows_ld * a.H;      // (row, head) records per split
+    const size_t rec = (size_t)row * a.H + h;
     float mx = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s)
-        mx = fmaxf(mx, a.mlpart[(((size_t)s * a.rows_ld + row) * a.H + h) * 2]);
-    float l = 0.f, o = 0.f;
-    for (int s = 0; s < a.nsplit; ++s) {
-        const float* ml = a.mlpart + (((size_t)s * a.rows_ld + row) * a.H + h) * 2;
-        if (ml[0] == -INFINITY) continue;
-        const float w = exp2f(ml[0] - mx);
-        l += ml[1] * w;
-        o += a.opart[(((size_t)s * a.rows_ld + row) * a.H + h) * DH + dim] * w;
+    for (int s = 0; s < a.nsplit; ++s) mx = fmaxf(mx, a.mlpart[(s * stride_s + rec) * 2]);
+    float L = 0.f;
+    for (int d0 = 4 * l; d0 < DH; d0 += 128) {
+        float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+        L = 0.f;
+        for (int s = 0; s < a.nsplit; ++s) {
+            const float2 ml = *(const float2*)(a.mlpart + (s * stride_s + rec) * 2);
+            if (ml.x == -INFINITY) continue;
+            const float w = exp2f(ml.x - mx);
+            L += ml.y * w;
+            const float4 v = *(const float4*)(a.opart + (s * stride_s + rec) * DH + d0);
+            o.x += v.x * w; o.y += v.y * w; o.z += v.z * w; o.w += v.w * w;
+        }
+        const float inv = 1.f / L;
+        xfrag_store4<XF32>(a.o, row, h * DH + d0, a.KCx, make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv));
     }
-    xfrag_store<XF32>(a.o, row, h * DH + dim, a.KCx, o / l);
 }
 
 // fp32 path (small models): one wave per (row, head); lanes stride over keys with

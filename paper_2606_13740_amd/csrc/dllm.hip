@@ -430,8 +430,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
 #undef ATTN_QG
 #undef ATTN
                 if (at.nsplit > 1) {
-                    const int total = Mc * H * Dh;
-                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(total, 256)), dim3(256), 0, s, at,
+                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(Mc * H, 8)), dim3(256), 0, s, at,
                                        Mc, Dh);
                 }
             }
