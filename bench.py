@@ -42,6 +42,25 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# The dominant kernel's measured HBM bytes come from the committed rocprofv3 counter
+# summary of this workload (FETCH_SIZE / WRITE_SIZE scaled by a 1 GiB copy).
+COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters_llada8b_bf16_p512_w32.txt")
+DOMINANT = "gemm_kernel<1, 6, 1, 8, 2, dllm::EpiSwiGLU<false> >"
+
+
+def measured_traffic(workload):
+    if workload != DEFAULT or not os.path.exists(COUNTERS):
+        return None
+    for line in open(COUNTERS):
+        if DOMINANT in line:
+            parts = line.split()
+            try:
+                return (float(parts[-2]) + float(parts[-1])) * 1e6
+            except ValueError:
+                return None
+    return None
+
+
 def cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob):
     """Oracle (float64 NumPy) on a bounded sample: one layer of the step plus the
     full LM head, scaled to the whole 32-layer step."""
@@ -163,9 +182,10 @@ def main():
     busy_ms = sum(v["launches_per_step"] * v["mean_us"] / 1e3 for v in kern.values())
     dom = "gateup"
     dk = kern[dom]
+    traffic = measured_traffic(args.workload)
     roof = {"bound": "hbm", "achieved": round(dk["gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "gemm gate/up + SwiGLU",
-            "alg_bytes_per_launch": dk["alg_bytes"]}
+            "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": "gemm gate/up + SwiGLU",
+            "alg_bytes_per_launch": dk["alg_bytes"], "mean_launch_us": round(dk["mean_us"], 2)}
 
     out = {
         "metric": "denoising steps/sec + tokens/sec, LLaDA-8B shape, block 32; % of HBM roofline",

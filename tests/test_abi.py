@@ -1,0 +1,108 @@
+"""The C ABI without a GPU: the library loads, exports every function the header
+declares, and rejects bad arguments on the host before any GPU work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dllm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dllm_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def dl():
+    import paper_2606_13740_amd as pkg
+    try:
+        pkg.lib()
+    except ImportError:
+        pytest.skip("libdllm.so not built")
+    return pkg
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("dllm_denoise_step", "dllm_commit", "dllm_append_prefix_kv", "dllm_refresh_kv",
+                     "dllm_prefill", "dllm_model_create", "dllm_kv_create"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(dl):
+    lib = ctypes.CDLL(dl.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_wraps_every_declared_symbol(dl):
+    missing = [n for n in declared_functions() if n not in dl._SIGNATURES]
+    assert not missing, missing
+
+
+def _create(dl, cfg):
+    h = ctypes.c_void_p()
+    rc = dl.lib().dllm_model_create(ctypes.byref(cfg), None, None, ctypes.byref(h))
+    return rc, dl.lib().dllm_last_error().decode()
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 48, -1),          # d_model != heads * head_dim
+    ("mask_id", 1024, -1),         # outside the vocabulary
+    ("max_window", 0, -1),
+    ("max_window", 257, -1),
+    ("dtype", 7, -3),
+    ("eps", 0.0, -1),
+    ("block", 0, -1),
+])
+def test_model_create_validates_config(dl, field, value, code):
+    cfg = dl.make_config(synth.TINY, "f32")
+    setattr(cfg, field, value)
+    rc, msg = _create(dl, cfg)
+    assert rc == code and msg
+
+
+def test_model_create_rejects_null_weights(dl):
+    cfg = dl.make_config(synth.TINY, "f32")
+    rc, msg = _create(dl, cfg)
+    assert rc == dl.DLLM_E_INVAL and "weights" in msg
+
+
+def test_bf16_head_dim_support_is_checked(dl):
+    cfg = dl.make_config(synth.MICRO, "bf16")       # head_dim 32: fp32 only
+    rc, _ = _create(dl, cfg)
+    assert rc == dl.DLLM_E_DTYPE
+
+
+@pytest.mark.parametrize("args,code", [
+    ((1, 1, 1, 1, 0, 4, -1), -1),        # k < 0
+    ((1, 1, 1, 1, -1, 4, 1), -1),        # seg_begin < 0
+    ((1, 1, 1, 1, 0, 2000, 1), -1),      # segment too long
+    ((None, 1, 1, 1, 0, 4, 1), -1),      # null pointer
+])
+def test_commit_validates_on_host(dl, args, code):
+    rc = dl.lib().dllm_commit(*args, None, None, None)
+    assert rc == code and dl.lib().dllm_last_error()
+
+
+def test_null_handles_are_rejected(dl):
+    L = dl.lib()
+    n = ctypes.c_size_t()
+    assert L.dllm_kv_bytes(None, 16, ctypes.byref(n)) == dl.DLLM_E_INVAL
+    assert L.dllm_denoise_step(None, None, None, None, 32, None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_append_prefix_kv(None, None, None, 32, None) == dl.DLLM_E_INVAL
+    assert L.dllm_refresh_kv(None, None, None, None, 4, None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_prefill(None, None, None, 4, None) == dl.DLLM_E_INVAL
+    assert L.dllm_kv_set_prefix_len(None, 0) == dl.DLLM_E_INVAL
+    assert L.dllm_model_destroy(None) == dl.DLLM_OK
+    assert L.dllm_kv_destroy(None) == dl.DLLM_OK
+
+
+def test_version_string(dl):
+    assert dl.lib().dllm_version().startswith(b"dllm")
