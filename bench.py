@@ -36,6 +36,67 @@ WORKLOADS = {
                                       masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)]),
 }
 DEFAULT = "llada8b_bf16_p512_w32"
+E2E = "llada8b_bf16_e2e128"      # end-to-end 128-token generation (prefill included)
+
+
+def run_e2e(args, dl, torch, shape, dev):
+    """Prompt 512 ids; 4 blocks of 32 decoded left to right, 32 denoising steps per
+    block with one commit each; after each block: append it to the prefix and
+    refresh 4 seeded positions of it with seeded new ids.  Wall-clock latency of the
+    whole generation (prefill included), after one untimed warmup generation."""
+    P0, B, S, R = 512, shape.block, 32, 4
+    glob = synth.global_weights(shape, "bf16")
+    model = dl.Model(shape, "bf16", glob, lambda l: synth.layer_weights(shape, l, "bf16"), max_window=64,
+                     max_pos=P0 + 4 * B + 64)
+    kv = dl.KVCache(model, P0 + 4 * B)
+    prompt = torch.from_numpy(synth.prompt_ids(shape, P0)).to(dev)
+    picks = [synth.refresh_picks(shape, P0 + b * B, B, R, call=b) for b in range(4)]
+    d_picks = [(torch.from_numpy(p).to(dev), torch.from_numpy(n).to(dev)) for p, n in picks]
+    tok0, mask0 = synth.window(shape, B, range(B))
+    d_tok0, d_mask0 = torch.from_numpy(tok0).to(dev), torch.from_numpy(mask0).to(dev)
+    ids = torch.empty(B, dtype=torch.int32, device=dev)
+    conf = torch.empty(B, device=dev)
+    rid = torch.empty(R, dtype=torch.int32, device=dev)
+    rconf = torch.empty(R, device=dev)
+    sched = [B // S + (1 if t < B % S else 0) for t in range(S)]
+
+    def generate():
+        dl.dllm_prefill(model.handle, kv.handle, prompt, P0)
+        for b in range(4):
+            tok, mask = d_tok0.clone(), d_mask0.clone()
+            for t in range(S):
+                dl.dllm_denoise_step(model.handle, kv.handle, tok, mask, B, ids, conf)
+                dl.dllm_commit(conf, ids, tok, mask, 0, B, sched[t])
+            dl.dllm_append_prefix_kv(model.handle, kv.handle, tok, B)
+            p, n = d_picks[b]
+            dl.dllm_refresh_kv(model.handle, kv.handle, p, n, R, rid, rconf)
+        torch.cuda.synchronize()
+
+    def fresh_kv():
+        nonlocal kv
+        kv.close()
+        kv = dl.KVCache(model, P0 + 4 * B)
+
+    generate()                                  # warmup (untimed)
+    times = []
+    for _ in range(3):
+        fresh_kv()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        generate()
+        times.append(time.perf_counter() - t0)
+    lat = min(times)
+    kv.close()
+    model.close()
+    return {
+        "metric": "end-to-end 128-token generation latency, LLaDA-8B shape, block 32",
+        "value": round(128 / lat, 2), "unit": "tokens/s", "n_gpus": 1, "steps": 128, "warmup": 128,
+        "ms_per_step": round(lat * 1000 / 128, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
+        "config": {"workload": E2E, "prompt": P0, "blocks": 4, "block": B, "steps_per_block": S,
+                   "refresh_per_block": R},
+        "latency_s": round(lat, 4), "latencies_s": [round(t, 4) for t in times],
+    }
 
 
 def log(*a):
@@ -91,7 +152,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS) + [E2E])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 launches): the reference for HBM byte counters")
@@ -114,6 +175,10 @@ def main():
 
     import paper_2606_13740_amd as dl
 
+    if args.workload == E2E:
+        torch.cuda.set_device(0)
+        print(json.dumps(run_e2e(args, dl, torch, synth.LLADA_8B, torch.device("cuda:0"))), flush=True)
+        return
     wl = WORKLOADS[args.workload]
     shape = synth.PRESETS[wl["shape"]]
     dtype = wl["dtype"]
