@@ -233,27 +233,40 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
 // per 256-thread workgroup.
 template <bool XF32>
 __global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a, int rows, int DH) {
+    constexpr int MAXS = 16;                                   // = the runtime's split cap
     const int pair = blockIdx.x * 8 + (threadIdx.x >> 5);
     const int l = threadIdx.x & 31;
     if (pair >= rows * a.H) return;
     const int h = pair % a.H, row = pair / a.H;
-    const size_t stride_s = (size_t)a.rows_ld * a.H;      // (row, head) records per split
+    const size_t stride_s = (size_t)a.rows_ld * a.H;          // (row, head) records per split
     const size_t rec = (size_t)row * a.H + h;
+    // issue every split's loads before using any of them
+    float2 ml[MAXS];
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s)
+        ml[s] = (s < a.nsplit) ? *(const float2*)(a.mlpart + (s * stride_s + rec) * 2)
+                               : make_float2(-INFINITY, 0.f);
     float mx = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s) mx = fmaxf(mx, a.mlpart[(s * stride_s + rec) * 2]);
-    float L = 0.f;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) mx = fmaxf(mx, ml[s].x);
+    float w[MAXS], L = 0.f;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) {
+        w[s] = (ml[s].x == -INFINITY) ? 0.f : exp2f(ml[s].x - mx);
+        L += ml[s].y * w[s];
+    }
+    const float inv = 1.f / L;
     for (int d0 = 4 * l; d0 < DH; d0 += 128) {
+        float4 v[MAXS];
+#pragma unroll
+        for (int s = 0; s < MAXS; ++s)
+            v[s] = (s < a.nsplit) ? *(const float4*)(a.opart + (s * stride_s + rec) * DH + d0)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
         float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-        L = 0.f;
-        for (int s = 0; s < a.nsplit; ++s) {
-            const float2 ml = *(const float2*)(a.mlpart + (s * stride_s + rec) * 2);
-            if (ml.x == -INFINITY) continue;
-            const float w = exp2f(ml.x - mx);
-            L += ml.y * w;
-            const float4 v = *(const float4*)(a.opart + (s * stride_s + rec) * DH + d0);
-            o.x += v.x * w; o.y += v.y * w; o.z += v.z * w; o.w += v.w * w;
+#pragma unroll
+        for (int s = 0; s < MAXS; ++s) {
+            o.x += v[s].x * w[s]; o.y += v[s].y * w[s]; o.z += v[s].z * w[s]; o.w += v[s].w * w[s];
         }
-        const float inv = 1.f / L;
         xfrag_store4<XF32>(a.o, row, h * DH + d0, a.KCx, make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv));
     }
 }

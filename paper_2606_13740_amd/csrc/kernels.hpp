@@ -93,10 +93,15 @@ residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
         if (n < d && m < M) {
             float4* xp = (float4*)(x + (size_t)m * d + n);
+            float4 p[8];
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks)
+                p[ks] = (ks < KS) ? *(const float4*)(P + ((size_t)ks * prow + m) * d + n)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
             v = *xp;
-            for (int ks = 0; ks < KS; ++ks) {
-                const float4 p = *(const float4*)(P + ((size_t)ks * prow + m) * d + n);
-                v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) {
+                v.x += p[ks].x; v.y += p[ks].y; v.z += p[ks].z; v.w += p[ks].w;
             }
             *xp = v;
         }
@@ -126,7 +131,16 @@ lm_combine_kernel(const LmPartial* part, int n_wg, int part_ld, int* out_id, flo
     const int m = blockIdx.x;
     const int lane = threadIdx.x;
     LmPartial acc{-INFINITY, -1, 0.f, 0.f};
-    for (int w = lane; w < n_wg; w += 64) acc = lm_merge(acc, part[(size_t)w * part_ld + m]);
+    for (int w0 = lane; w0 < n_wg; w0 += 64 * 8) {
+        LmPartial q[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int w = w0 + 64 * j;
+            q[j] = (w < n_wg) ? part[(size_t)w * part_ld + m] : LmPartial{-INFINITY, -1, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = lm_merge(acc, q[j]);
+    }
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
         LmPartial o;
