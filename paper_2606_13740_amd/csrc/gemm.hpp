@@ -45,6 +45,14 @@ constexpr int pipeline_depth() {
     return d < 1 ? 1 : (d > 8 ? 8 : d);
 }
 
+// Reduction slots: the largest power of two <= NWk whose slots fit the budget.
+template <int NWk>
+constexpr int reduce_slots(int slot_bytes) {
+    int s = NWk;
+    while (s > 1 && s * slot_bytes > 100 * 1024) s >>= 1;
+    return s;
+}
+
 // Workgroup layout: NWn x NWk waves.  Wave (wn, wk) streams FW row tiles (group
 // wn) over slice wk of the workgroup's K range; the NWk slices of a group are
 // summed in LDS in a fixed order.  grid = (row groups / NWn, KS, token blocks):
@@ -60,7 +68,11 @@ gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int D = pipeline_depth<WT, FW, MT>();
     constexpr int NW = NWn * NWk;
     constexpr int NR = 16 * FW, MR = 16 * MT, LDY = MR + 1;
-    __shared__ float Y[NWn][NR * LDY];
+    // K-slice partials: S slots per row group (S <= NWk, a power of two that keeps
+    // the workgroup's slots within ~100 KiB of LDS); slot 0 ends with the sum.
+    constexpr int SLOT = NR * LDY;
+    constexpr int S = reduce_slots<NWk>(NWn * SLOT * 4);
+    __shared__ float Y[NWn][S * SLOT];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -147,19 +159,33 @@ gemm_kernel(GemmArgs g, Epi epi) {
         }
     }
 
-    // Sum the NWk K-slices of each row group into Y[wn], slice by slice (fixed order).
+    // Sum the NWk K-slices of each row group into Y[wn] in a fixed order: wave wk
+    // adds into slot wk % S (rounds of S waves), then every thread sums the S
+    // slots of its elements in slot order.
     const int r = lane & 15, gq = lane >> 4;
-    for (int k = 0; k < NWk; ++k) {
-        if (wk == k) {
+    for (int k0 = 0; k0 < NWk; k0 += S) {
+        if (wk >= k0 && wk < k0 + S) {
+            float* slot = &Y[wn][(wk - k0) * SLOT];
 #pragma unroll
             for (int f = 0; f < FW; ++f)
 #pragma unroll
                 for (int t = 0; t < MT; ++t)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        float* p = &Y[wn][(16 * f + 4 * gq + i) * LDY + 16 * t + r];
-                        *p = (k == 0) ? acc[f][t][i] : *p + acc[f][t][i];
+                        float* p = slot + (16 * f + 4 * gq + i) * LDY + 16 * t + r;
+                        *p = (k0 == 0) ? acc[f][t][i] : *p + acc[f][t][i];
                     }
+        }
+        __syncthreads();
+    }
+    if constexpr (S > 1) {
+        for (int idx = threadIdx.x; idx < NWn * NR * MR; idx += blockDim.x) {
+            const int q = idx / (NR * MR), e = idx % (NR * MR);
+            const int o = (e / MR) * LDY + e % MR;
+            float v = Y[q][o];
+#pragma unroll
+            for (int sl = 1; sl < S; ++sl) v += Y[q][sl * SLOT + o];
+            Y[q][o] = v;
         }
         __syncthreads();
     }
