@@ -77,7 +77,7 @@ struct Workspace {
 };
 
 constexpr int MAX_SPLIT = 16;
-constexpr int RES_SPLIT = 8;     // K slices of the O / down projections for windows of <= 64 rows
+constexpr int RES_SPLIT = 4;     // K slices of the O / down projections for windows of <= 64 rows
 
 }  // namespace
 
@@ -133,7 +133,7 @@ int pick_MT(int M) {
 //   QKV    3 row tiles per workgroup, K split over 8 waves          (4.3 TB/s)
 //   gate/up 6 row tiles per workgroup, K split over 8 waves         (5.2 TB/s)
 //   LM head 4 waves x 8 row tiles, each wave streams the whole K    (6.3 TB/s)
-//   O/down 4 row tiles, K split over 4 waves x 8 workgroups (split-K) + reduction
+//   O/down 4 row tiles, K split over 8 waves x 4 workgroups (split-K) + reduction
 // Small models (fewer row tiles than CUs x tiles) use one tile per workgroup.
 bool big(GemmKind k, int n_tiles) {
     switch (k) {
@@ -184,7 +184,7 @@ int launch_gemm(int n_tiles, int MT, int KS, const GemmArgs& g, const Epi& epi, 
         if (b) return launch_gemm_mt<WT, 8, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
         return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
     } else {
-        if (b) return launch_gemm_mt<WT, 4, 1, 4>(MT, g, epi, n_tiles, KS, gy, s);
+        if (b) return launch_gemm_mt<WT, 4, 1, 8>(MT, g, epi, n_tiles, KS, gy, s);
         return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, KS, gy, s);
     }
 }
