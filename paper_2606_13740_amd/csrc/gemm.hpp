@@ -30,7 +30,11 @@ struct GemmArgs {
 };
 
 // Epilogue interface:
-//   __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int part) const
+//   static constexpr int kSmem                      LDS bytes the epilogue keeps per row group
+//   void prologue(char* sm, int n0, int nrows, int m0, int mcols) const
+//       called by every thread at kernel start (e.g. to stage tables in sm while
+//       the weights stream)
+//   void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int part, char* sm) const
 // Y is LDS [nrows][ldy] holding final outputs of weight rows [n0, n0 + nrows) for
 // tokens [m0, m0 + mcols) (int8 row scales applied); every thread of the
 // workgroup calls it (it may use __syncthreads and overwrite Y); `part` numbers
@@ -73,6 +77,8 @@ gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int SLOT = NR * LDY;
     constexpr int S = reduce_slots<NWk>(NWn * SLOT * 4);
     __shared__ float Y[NWn][S * SLOT];
+    constexpr int ESM = Epi::kSmem > 0 ? Epi::kSmem : 16;
+    __shared__ __align__(16) char esm[NWn * ESM];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -81,6 +87,13 @@ gemm_kernel(GemmArgs g, Epi epi) {
     const int KS = gridDim.y;
     const int kb0 = (int)(((long)blockIdx.y * g.KCw) / KS);
     const int kb1 = (int)(((long)(blockIdx.y + 1) * g.KCw) / KS);
+
+#pragma unroll
+    for (int q = 0; q < NWn; ++q) {
+        const int nq0 = (blockIdx.x * NWn + q) * FW;
+        const int nfq = max(0, min(FW, g.n_tiles - nq0));
+        if (nfq > 0) epi.prologue(esm + q * ESM, nq0 * 16, nfq * 16, mt0 * 16, MR);
+    }
 
     f32x4_t acc[FW][MT];
 #pragma unroll
@@ -202,7 +215,7 @@ gemm_kernel(GemmArgs g, Epi epi) {
             }
             __syncthreads();
         }
-        epi(Y[q], LDY, nt0 * 16, nf * 16, mt0 * 16, MR, blockIdx.x * NWn + q);
+        epi(Y[q], LDY, nt0 * 16, nf * 16, mt0 * 16, MR, blockIdx.x * NWn + q, esm + q * ESM);
         __syncthreads();
     }
 }
@@ -230,6 +243,9 @@ struct EpiQKV {
     size_t kv_plane;
     int Cs;
 
+    static constexpr int kPairs = 24 * 64;          // staged (cos, sin): 3 row tiles x 64 tokens
+    static constexpr int kSmem = kPairs * 8;
+
     __device__ __forceinline__ static void put(T* p, size_t plane, float v) {
         if constexpr (XF32) {
             *p = v;
@@ -241,11 +257,31 @@ struct EpiQKV {
         }
     }
 
-    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int) const {
+    // (cos, sin) of every (pair, token) of the group's Q/K rows, fetched while the weights stream
+    __device__ void prologue(char* sm, int n0, int nrows, int m0, int mcols) const {
         const int npairs = nrows >> 1;
-        const int half = Dh >> 1;
+        if (npairs * mcols > kPairs) return;
+        float2* cs = (float2*)sm;
         for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
             const int p = idx % npairs, ml = idx / npairs;
+            const int m = m0 + ml, n = n0 + 2 * p;
+            if (m >= M || n >= 2 * d) continue;
+            const int rr = (n % d) % Dh;
+            const int ps = pos ? pos[m] : pos_base + m;
+            cs[idx] = rope[(size_t)ps * (Dh >> 1) + (rr >> 1)];
+        }
+    }
+
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int, char* sm) const {
+        const int npairs = nrows >> 1;
+        const int half = Dh >> 1;
+        const bool staged = npairs * mcols <= kPairs;
+        // V^T rows are contiguous along the token axis: there consecutive threads take consecutive tokens
+        const bool vt = n0 >= 2 * d;
+        const float2* csm = (const float2*)sm;
+        for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
+            const int p = vt ? idx / mcols : idx % npairs;
+            const int ml = vt ? idx % mcols : idx / npairs;
             const int m = m0 + ml;
             if (m >= M) continue;
             const int n = n0 + 2 * p;
@@ -255,7 +291,7 @@ struct EpiQKV {
             const int h = nn / Dh, rr = nn - h * Dh;
             if (seg < 2) {
                 const int j = rr >> 1;
-                const float2 cs = rope[(size_t)ps * half + j];
+                const float2 cs = staged ? csm[p + npairs * ml] : rope[(size_t)ps * half + j];
                 const float ra = a * cs.x - b * cs.y;
                 const float rb = a * cs.y + b * cs.x;
                 if (seg == 0) {
@@ -279,14 +315,19 @@ struct EpiQKV {
 // Split-K partial results: P[ks][m][n] = Y[n][m] (a reduction kernel finishes them).
 struct EpiPartial {
     float* P;
-    int ldn;                // row length of P (>= packed rows)
+    int ldn;                // row length of P (>= packed rows, a multiple of 4)
     int rows;               // token rows per K slice of P
 
-    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int) const {
+    static constexpr int kSmem = 0;
+    __device__ void prologue(char*, int, int, int, int) const {}
+
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int, char*) const {
         float* base = P + (size_t)blockIdx.y * rows * ldn;
-        for (int idx = threadIdx.x; idx < nrows * mcols; idx += blockDim.x) {
-            const int nl = idx % nrows, ml = idx / nrows;
-            base[(size_t)(m0 + ml) * ldn + n0 + nl] = Y[nl * ldy + ml];
+        const int nq = nrows >> 2;
+        for (int idx = threadIdx.x; idx < nq * mcols; idx += blockDim.x) {
+            const int qd = idx % nq, ml = idx / nq;
+            const float* y = Y + (4 * qd) * ldy + ml;
+            *(float4*)(base + (size_t)(m0 + ml) * ldn + n0 + 4 * qd) = make_float4(y[0], y[ldy], y[2 * ldy], y[3 * ldy]);
         }
     }
 };
@@ -298,13 +339,21 @@ struct EpiSwiGLU {
     void* a;
     int KCx;
 
-    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int) const {
-        const int npairs = nrows >> 1;
-        for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
-            const int p = idx % npairs, ml = idx / npairs;
-            const float gt = Y[(2 * p) * ldy + ml], up = Y[(2 * p + 1) * ldy + ml];
-            const float act = gt / (1.0f + expf(-gt)) * up;
-            xfrag_store<XF32>(a, m0 + ml, (n0 >> 1) + p, KCx, act);
+    static constexpr int kSmem = 0;
+    __device__ void prologue(char*, int, int, int, int) const {}
+
+    // four consecutive outputs (eight packed rows) per thread
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int, char*) const {
+        const int nq = nrows >> 3;
+        for (int idx = threadIdx.x; idx < nq * mcols; idx += blockDim.x) {
+            const int qd = idx % nq, ml = idx / nq;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float gt = Y[(8 * qd + 2 * e) * ldy + ml], up = Y[(8 * qd + 2 * e + 1) * ldy + ml];
+                v[e] = gt / (1.0f + expf(-gt)) * up;
+            }
+            xfrag_store4<XF32>(a, m0 + ml, (n0 >> 1) + 4 * qd, KCx, make_float4(v[0], v[1], v[2], v[3]));
         }
     }
 };
@@ -318,14 +367,27 @@ struct LmPartial {
     float pad;
 };
 
+// Merge of two (max, lowest argmax, sum exp) records; symmetric in its operands.
+__device__ __forceinline__ LmPartial lm_merge_fast(LmPartial a, LmPartial b) {
+    if (b.arg < 0) return a;
+    if (a.arg < 0) return b;
+    const float mx = fmaxf(a.mx, b.mx);
+    const int arg = (a.mx > b.mx) ? a.arg : (b.mx > a.mx ? b.arg : min(a.arg, b.arg));
+    return LmPartial{mx, arg, a.s * __expf(a.mx - mx) + b.s * __expf(b.mx - mx), 0.f};
+}
+
 struct EpiLM {
     int V, mask_id, M;
     LmPartial* part;        // [n_groups][part_ld]
     int part_ld;
     float* logits;          // [M][V] or nullptr
 
-    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int grp) const {
-        __shared__ LmPartial red[8][64];
+    static constexpr int kSmem = 0;
+    __device__ void prologue(char*, int, int, int, int) const {}
+
+    // TPT consecutive lanes per token, each an online (max, argmax, sum exp) over a
+    // slice of the rows, then a fixed shuffle tree over the slices.
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int grp, char*) const {
         if (logits != nullptr) {
             for (int idx = threadIdx.x; idx < nrows * mcols; idx += blockDim.x) {
                 const int nl = idx % nrows, ml = idx / nrows;
@@ -334,41 +396,32 @@ struct EpiLM {
                     logits[(size_t)m * V + n] = (n == mask_id) ? -INFINITY : Y[nl * ldy + ml];
             }
         }
-        // slice s of the rows for token column ml; 8 slices per column
-        const int per = (nrows + 7) >> 3;
-        for (int idx = threadIdx.x; idx < 8 * mcols; idx += blockDim.x) {
-            const int ml = idx % mcols, sl = idx / mcols;
-            const int b = sl * per, e = min(nrows, b + per);
-            float mx = -INFINITY;
-            int arg = -1;
-            for (int nl = b; nl < e; ++nl) {
-                const int n = n0 + nl;
-                if (n >= V || n == mask_id) continue;
-                const float v = Y[nl * ldy + ml];
-                if (v > mx) { mx = v; arg = n; }
+        const int tpt = blockDim.x / mcols;          // a power of two dividing 64
+        const int ml = threadIdx.x / tpt, sl = threadIdx.x % tpt;
+        const int per = (nrows + tpt - 1) / tpt;
+        const int b = sl * per, e = min(nrows, b + per);
+        LmPartial a{-INFINITY, -1, 0.f, 0.f};
+        for (int nl = b; nl < e; ++nl) {
+            const int n = n0 + nl;
+            if (n >= V || n == mask_id) continue;
+            const float v = Y[nl * ldy + ml];
+            if (v > a.mx) {
+                a.s = (a.arg < 0 ? 0.f : a.s * __expf(a.mx - v)) + 1.f;
+                a.mx = v;
+                a.arg = n;
+            } else {
+                a.s += __expf(v - a.mx);
             }
-            float s = 0.f;
-            if (arg >= 0)
-                for (int nl = b; nl < e; ++nl) {
-                    const int n = n0 + nl;
-                    if (n >= V || n == mask_id) continue;
-                    s += __expf(Y[nl * ldy + ml] - mx);
-                }
-            red[sl][ml] = LmPartial{mx, arg, s, 0.f};
         }
-        __syncthreads();
-        for (int ml = threadIdx.x; ml < mcols; ml += blockDim.x) {
-            LmPartial a = red[0][ml];
-            for (int sl = 1; sl < 8; ++sl) {
-                const LmPartial b = red[sl][ml];
-                if (b.arg < 0) continue;
-                if (a.arg < 0) { a = b; continue; }
-                const float mx = fmaxf(a.mx, b.mx);
-                const int arg = (a.mx > b.mx) ? a.arg : (b.mx > a.mx ? b.arg : min(a.arg, b.arg));
-                a = LmPartial{mx, arg, a.s * __expf(a.mx - mx) + b.s * __expf(b.mx - mx), 0.f};
-            }
-            part[(size_t)grp * part_ld + m0 + ml] = a;
+        for (int off = 1; off < tpt; off <<= 1) {
+            LmPartial o;
+            o.mx = __shfl_xor(a.mx, off);
+            o.arg = __shfl_xor(a.arg, off);
+            o.s = __shfl_xor(a.s, off);
+            o.pad = 0.f;
+            a = lm_merge_fast(a, o);
         }
+        if (sl == 0) part[(size_t)grp * part_ld + m0 + ml] = a;
     }
 };
 
