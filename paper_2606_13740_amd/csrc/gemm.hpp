@@ -272,16 +272,74 @@ struct EpiQKV {
         }
     }
 
+    // four consecutive values of one plane pair (fp32: one 16-byte store; bf16: 8-byte hi and lo stores)
+    __device__ __forceinline__ static void put4(T* p, size_t plane, const float (&v)[4]) {
+        if constexpr (XF32) {
+            *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+            uint16_t h[4], l[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) split_bf16(v[e], h[e], l[e]);
+            *(uint2*)p = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+            *(uint2*)(p + plane) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+        }
+    }
+
     __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int, char* sm) const {
         const int npairs = nrows >> 1;
         const int half = Dh >> 1;
         const bool staged = npairs * mcols <= kPairs;
-        // V^T rows are contiguous along the token axis: there consecutive threads take consecutive tokens
-        const bool vt = n0 >= 2 * d;
         const float2* csm = (const float2*)sm;
+        if (n0 + nrows <= 2 * d) {
+            // Q / K rows: four consecutive RoPE pairs (dims j..j+3 and j+half..j+half+3) per thread
+            const int nq = npairs >> 2;
+            for (int idx = threadIdx.x; idx < nq * mcols; idx += blockDim.x) {
+                const int qd = idx % nq, ml = idx / nq;
+                const int m = m0 + ml;
+                if (m >= M) continue;
+                const int p0 = 4 * qd, n = n0 + 2 * p0;
+                const int ps = pos ? pos[m] : pos_base + m;
+                const int seg = n / d, nn = n - seg * d;
+                const int h = nn / Dh, j0 = (nn - h * Dh) >> 1;
+                float ra[4], rb[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float a = Y[(2 * (p0 + e)) * ldy + ml], b = Y[(2 * (p0 + e) + 1) * ldy + ml];
+                    const float2 cs = staged ? csm[p0 + e + npairs * ml] : rope[(size_t)ps * half + j0 + e];
+                    ra[e] = a * cs.x - b * cs.y;
+                    rb[e] = a * cs.y + b * cs.x;
+                }
+                T* dst = (seg == 0) ? q + (size_t)m * d + h * Dh : Kc + ((size_t)h * Cs + ps) * Dh;
+                const size_t plane = (seg == 0) ? q_plane : kv_plane;
+                put4(dst + j0, plane, ra);
+                put4(dst + j0 + half, plane, rb);
+            }
+            return;
+        }
+        if (n0 >= 2 * d && pos == nullptr && ((pos_base + m0) & 3) == 0) {
+            // V^T rows, consecutive positions: four tokens per thread along the row; a
+            // quad that reaches past the last real row falls back to single stores
+            const int nt = mcols >> 2;
+            for (int idx = threadIdx.x; idx < nrows * nt; idx += blockDim.x) {
+                const int tq = idx % nt, nl = idx / nt;
+                const int m = m0 + 4 * tq;
+                if (m >= M) continue;
+                const int nn = n0 + nl - 2 * d;
+                const int h = nn / Dh, rr = nn - h * Dh;
+                T* dst = Vt + ((size_t)h * Dh + rr) * Cs + pos_base + m;
+                const float* y = Y + nl * ldy + 4 * tq;
+                if (m + 3 < M) {
+                    const float v[4] = {y[0], y[1], y[2], y[3]};
+                    put4(dst, kv_plane, v);
+                } else {
+                    for (int e = 0; e < 4 && m + e < M; ++e) put(dst + e, kv_plane, y[e]);
+                }
+            }
+            return;
+        }
+        // general case (a group across the K/V boundary, or explicit positions)
         for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
-            const int p = vt ? idx / mcols : idx % npairs;
-            const int ml = vt ? idx % mcols : idx / npairs;
+            const int p = idx % npairs, ml = idx / npairs;
             const int m = m0 + ml;
             if (m >= M) continue;
             const int n = n0 + 2 * p;
