@@ -61,8 +61,8 @@ extern "C" {
 
 /* Weight / arithmetic types. */
 #define DLLM_F32 0   /* fp32 weights, fp32 activations and KV cache */
-#define DLLM_BF16 1  /* bf16 weights, bf16 GEMM operands and KV cache, fp32 accumulate */
-#define DLLM_W8 2    /* int8 weights with fp32 per-output-row scales, bf16 activations */
+#define DLLM_BF16 1  /* bf16 weights; activations, Q and the KV cache as bf16 hi/lo pairs; fp32 accumulate */
+#define DLLM_W8 2    /* int8 weights with fp32 per-output-row scales; activations as for DLLM_BF16 */
 
 typedef struct dllm_model dllm_model;
 typedef struct dllm_kv dllm_kv;
@@ -124,10 +124,16 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
                       dllm_model** out);
 int dllm_model_destroy(dllm_model* m);
 
-/* Bytes of device memory a KV cache of `capacity` positions needs.
- * Layout inside the caller's buffer, element type float (F32) or bfloat16:
- *   K   of layer l, head h, position p, dim j: ((l*2+0)*H + h)*cap*Dh + p*Dh + j
- *   V^T of layer l, head h, dim j, position p: ((l*2+1)*H + h)*Dh*cap + j*cap + p
+/* Bytes of device memory a KV cache of `capacity` positions needs (4 bytes per
+ * cached value).  Layout inside the caller's buffer, with Cs = capacity rounded
+ * up to a multiple of 32 and P = H*Cs*Dh elements per plane:
+ *   F32 models, element float, 2 planes per layer (K, V^T):
+ *     K   of layer l, head h, position p, dim j: (l*2+0)*P + (h*Cs + p)*Dh + j
+ *     V^T of layer l, head h, dim j, position p: (l*2+1)*P + (h*Dh + j)*Cs + p
+ *   BF16 / W8 models, element bfloat16, 4 planes per layer (K hi, K lo, V^T hi,
+ *   V^T lo); a value is hi + lo with hi = bf16(v), lo = bf16(v - hi):
+ *     K   hi / lo: (l*4+0)*P + ... / (l*4+1)*P + ...   (same offsets as above)
+ *     V^T hi / lo: (l*4+2)*P + ... / (l*4+3)*P + ...
  * K is stored after RoPE. */
 int dllm_kv_bytes(const dllm_model* m, int32_t capacity, size_t* bytes);
 
