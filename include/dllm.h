@@ -234,6 +234,14 @@ int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms);
  * express achieved bandwidth. */
 int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes);
 
+/* Measurement helper: one launch of a plain streaming read over `bytes` bytes of
+ * the device buffer d_buf (16-byte aligned; bytes a multiple of 16), the same
+ * 16-byte-per-lane non-temporal loads the GEMMs stream weights with.  The caller
+ * times it with events on `stream` to measure the achievable HBM read rate that
+ * the kernels' bandwidth is compared with.  d_sink (device, >= 4 bytes) receives a
+ * value only in a case that never occurs for real data; it keeps the loads alive. */
+int dllm_read_bandwidth(const void* d_buf, size_t bytes, uint32_t* d_sink, dllm_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

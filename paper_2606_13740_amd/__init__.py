@@ -68,6 +68,7 @@ _SIGNATURES = {
     "dllm_probe_enable": ([_vp, _i32, _i32], ctypes.c_int),
     "dllm_probe_read": ([_vp, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dllm_kernel_bytes": ([_vp, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "dllm_read_bandwidth": ([_vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
 }
 
 
@@ -196,6 +197,10 @@ def dllm_kernel_bytes(model: int, kernel_class: int, W: int, P: int) -> float:
     b = ctypes.c_double()
     _check(lib().dllm_kernel_bytes(model, kernel_class, W, P, ctypes.byref(b)), "dllm_kernel_bytes")
     return b.value
+
+
+def dllm_read_bandwidth(buf, nbytes: int, sink, stream=None):
+    _check(lib().dllm_read_bandwidth(_ptr(buf), nbytes, _ptr(sink), _stream(stream)), "dllm_read_bandwidth")
 
 
 # ----------------------------------------------------------------------------

@@ -822,4 +822,15 @@ int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int3
     return DLLM_OK;
 }
 
+int dllm_read_bandwidth(const void* d_buf, size_t bytes, uint32_t* d_sink, dllm_stream stream) {
+    if (!d_buf || !d_sink) return fail(DLLM_E_INVAL, "NULL argument");
+    if (((uintptr_t)d_buf & 15) != 0 || (bytes & 15) != 0)
+        return fail(DLLM_E_INVAL, "buffer must be 16-byte aligned and a multiple of 16 bytes");
+    if (bytes == 0) return DLLM_OK;
+    hipLaunchKernelGGL(read_stream_kernel, dim3(8192), dim3(256), 0, (hipStream_t)stream, (const u32x4_t*)d_buf,
+                       bytes / 16, d_sink);
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
 }  // extern "C"

@@ -110,6 +110,24 @@ residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps
     write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red);
 }
 
+// Streaming read of n 16-byte units (measurement helper): grid-stride, 4 loads in flight per lane.
+__global__ void __launch_bounds__(256) read_stream_kernel(const u32x4_t* p, size_t n, uint32_t* sink) {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    uint32_t acc = 0;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const u32x4_t a = ldg16_nt(p + i), b = ldg16_nt(p + i + stride);
+        const u32x4_t c = ldg16_nt(p + i + 2 * stride), d = ldg16_nt(p + i + 3 * stride);
+        acc ^= a[0] ^ a[1] ^ a[2] ^ a[3] ^ b[0] ^ b[1] ^ b[2] ^ b[3] ^ c[0] ^ c[1] ^ c[2] ^ c[3] ^ d[0] ^ d[1] ^
+               d[2] ^ d[3];
+    }
+    for (; i < n; i += stride) {
+        const u32x4_t a = ldg16_nt(p + i);
+        acc ^= a[0] ^ a[1] ^ a[2] ^ a[3];
+    }
+    if (acc == 0x9E3779B9u) *sink = acc;
+}
+
 // ---------------------------------------------------------------------------
 // LM-head merge across vocabulary tiles -> id, confidence = 1 / sum exp(l - max)
 // ---------------------------------------------------------------------------

@@ -104,5 +104,13 @@ def test_null_handles_are_rejected(dl):
     assert L.dllm_kv_destroy(None) == dl.DLLM_OK
 
 
+def test_read_bandwidth_validates_on_host(dl):
+    L = dl.lib()
+    assert L.dllm_read_bandwidth(None, 16, None, None) == dl.DLLM_E_INVAL
+    # misaligned buffer / size: rejected before any launch (the pointers are never dereferenced)
+    assert L.dllm_read_bandwidth(ctypes.c_void_p(0x1001), 16, ctypes.c_void_p(0x2000), None) == dl.DLLM_E_INVAL
+    assert L.dllm_read_bandwidth(ctypes.c_void_p(0x1000), 17, ctypes.c_void_p(0x2000), None) == dl.DLLM_E_INVAL
+
+
 def test_version_string(dl):
     assert dl.lib().dllm_version().startswith(b"dllm")
