@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE: imported only by the tests, the smoke check and the
 benchmark's CPU-baseline leg.  The product path never imports it.
 """
 from .model import (  # noqa: F401
-    OracleKV, OracleModel, StepOut, append_block, attend, attend_masked, block_causal_allowed,
-    commit, commit_schedule, confidence, denoise_step, dequantize_rows, forward_full,
+    IV, S, V, OracleKV, OracleModel, StepOut, append_block, attend, attend_masked, block_causal_allowed,
+    commit, commit_schedule, commit_staged, confidence, denoise_step, dequantize_rows, forward_full,
     forward_rows, input_ids, prefill, quantize_rows_int8, refresh, rmsnorm, rope, silu, softmax,
 )

@@ -379,6 +379,44 @@ def refresh(model: OracleModel, kv: OracleKV, pos: Sequence[int], new_ids: Seque
     return ids, conf, logits
 
 
+# Token states of staged stabilisation (System Design, "Staged Token Stabilization").
+IV, V, S = 0, 1, 2      # invisible (masked), visible (exposed, still revisable), stable
+
+
+def commit_staged(conf: np.ndarray, pred: np.ndarray, tok: np.ndarray, mask: np.ndarray, state: np.ndarray,
+                  seg_begin: int, seg_len: int, theta_visible: float, theta_stable: float):
+    """One step of staged token stabilisation over [seg_begin, seg_begin + seg_len)
+    (System Design, "Staged Token Stabilization"; thresholds 0.7 / 0.9 in the Evaluation
+    setup).
+
+    - Every invisible position whose confidence reaches theta_visible becomes visible:
+      it takes its predicted id and leaves the mask.
+    - If none did and invisible positions remain, the most confident of them becomes
+      visible (equal confidence -> lower position), so that decoding always progresses.
+    - Every visible position, the ones just promoted included, whose confidence reaches
+      theta_stable becomes stable.  A visible position keeps its id here: identity
+      revision of visible tokens goes through the refresh path.
+
+    Confidences and thresholds are compared in float32 (the precision the confidence
+    is produced in).  Returns the positions that left the invisible state, ascending.
+    """
+    c = np.asarray(conf, dtype=np.float32)
+    tv, ts = np.float32(theta_visible), np.float32(theta_stable)
+    seg = range(seg_begin, seg_begin + seg_len)
+    cand = [p for p in seg if state[p] == IV]
+    promoted = [p for p in cand if c[p] >= tv]
+    if not promoted and cand:
+        promoted = [min(cand, key=lambda p: (-float(c[p]), p))]
+    for p in promoted:
+        tok[p] = pred[p]
+        mask[p] = 0
+        state[p] = V
+    for p in seg:
+        if state[p] == V and c[p] >= ts:
+            state[p] = S
+    return np.array(sorted(promoted), dtype=np.int32)
+
+
 def commit_schedule(n_masked: int, steps: int) -> list:
     """Commits per step: floor(N / s) + [t < N mod s] for t = 0 .. s-1."""
     base, rem = divmod(n_masked, steps)

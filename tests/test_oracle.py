@@ -433,3 +433,97 @@ def test_synth_inputs_are_reproducible_and_sliceable():
     assert abs(f.std() - 0.02) < 2e-4 and abs(f.mean()) < 2e-4
     ids = synth.prompt_ids(synth.TINY, 5000)
     assert ids.min() >= 0 and ids.max() < synth.TINY.mask_id
+
+
+# ---- staged token stabilisation (System Design, "Staged Token Stabilization") ----
+
+def _staged_case(rng, n, ties=False):
+    conf = rng.random(n).astype(np.float32)
+    if ties:
+        conf = np.round(conf * 4).astype(np.float32) / 4
+    state = rng.integers(0, 3, n).astype(np.uint8)
+    mask = (state == oracle.IV).astype(np.uint8)
+    pred = rng.integers(0, 1000, n).astype(np.int32)
+    tok = np.where(mask == 1, 999, rng.integers(0, 1000, n)).astype(np.int32)
+    return conf, pred, tok, mask, state
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_commit_staged_postconditions(seed):
+    """Promoted set, state transitions and untouched positions, from set algebra."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 40))
+    conf, pred, tok, mask, state = _staged_case(rng, n, ties=bool(seed % 2))
+    b = int(rng.integers(0, n))
+    ln = int(rng.integers(1, n - b + 1))
+    tv, ts = float(rng.choice([0.0, 0.3, 0.5, 0.7, 1.5])), float(rng.choice([0.2, 0.6, 0.9, 2.0]))
+    tok0, mask0, state0 = tok.copy(), mask.copy(), state.copy()
+    got = oracle.commit_staged(conf, pred, tok, mask, state, b, ln, tv, ts)
+    seg = np.zeros(n, bool)
+    seg[b:b + ln] = True
+    iv = seg & (state0 == oracle.IV)
+    above = iv & (conf >= np.float32(tv))
+    if above.any():
+        want = set(np.flatnonzero(above))
+    elif iv.any():
+        idx = np.flatnonzero(iv)
+        best = idx[conf[idx] == conf[idx].max()].min()      # highest conf, then lowest position
+        want = {int(best)}
+    else:
+        want = set()
+    assert set(got.tolist()) == want and list(got) == sorted(got)
+    prom = np.zeros(n, bool)
+    prom[list(want)] = True
+    assert np.array_equal(tok, np.where(prom, pred, tok0))
+    assert np.array_equal(mask, np.where(prom, 0, mask0))
+    vis_after = prom | (state0 == oracle.V)
+    want_state = np.where(seg & vis_after & (conf >= np.float32(ts)), oracle.S,
+                          np.where(prom, oracle.V, state0))
+    assert np.array_equal(state, want_state.astype(np.uint8))
+    assert np.all(state >= state0)                             # states only move forward
+
+
+def test_commit_staged_high_threshold_is_top1_commit():
+    """theta_visible above every probability: one promotion per step, exactly the k=1 commit."""
+    rng = np.random.default_rng(7)
+    for _ in range(20):
+        n = 24
+        conf = (rng.integers(0, 6, n) / 8).astype(np.float32)     # many ties
+        pred = rng.integers(0, 50, n).astype(np.int32)
+        mask = (rng.random(n) < 0.6).astype(np.uint8)
+        state = np.where(mask == 1, oracle.IV, oracle.V).astype(np.uint8)
+        tok = np.where(mask == 1, 99, 5).astype(np.int32)
+        t2, m2 = tok.copy(), mask.copy()
+        got = oracle.commit_staged(conf, pred, tok, mask, state, 0, n, 1.5, 2.0)
+        ref = oracle.commit(conf, pred, t2, m2, 0, n, 1)
+        assert list(got) == list(ref) and np.array_equal(tok, t2) and np.array_equal(mask, m2)
+
+
+def test_commit_staged_zero_threshold_reveals_all():
+    n = 16
+    conf = np.linspace(0.01, 0.99, n).astype(np.float32)
+    pred = np.arange(n, dtype=np.int32) + 100
+    tok, mask = np.full(n, 7, np.int32), np.ones(n, np.uint8)
+    state = np.zeros(n, np.uint8)
+    got = oracle.commit_staged(conf, pred, tok, mask, state, 0, n, 0.0, 0.9)
+    assert list(got) == list(range(n)) and not mask.any() and np.array_equal(tok, pred)
+    assert np.array_equal(state, np.where(conf >= np.float32(0.9), oracle.S, oracle.V))
+
+
+def test_commit_staged_progress_and_stability():
+    """Every step promotes at least one invisible position, so a block of n finishes in
+    at most n steps; stable positions never change again."""
+    rng = np.random.default_rng(3)
+    n = 32
+    tok, mask, state = np.full(n, 1023, np.int32), np.ones(n, np.uint8), np.zeros(n, np.uint8)
+    for step in range(n):
+        conf = rng.random(n).astype(np.float32) ** 4
+        pred = rng.integers(0, 1000, n).astype(np.int32)
+        before_s = state == oracle.S
+        tok_s = tok.copy()
+        got = oracle.commit_staged(conf, pred, tok, mask, state, 0, n, 0.7, 0.9)
+        assert len(got) >= 1 or not (state == oracle.IV).any()
+        assert np.array_equal(tok[before_s], tok_s[before_s]) and np.all(state[before_s] == oracle.S)
+        if not mask.any():
+            break
+    assert not mask.any() and np.all(state != oracle.IV)
