@@ -234,6 +234,31 @@ int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms);
  * express achieved bandwidth. */
 int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes);
 
+/* Token states of staged stabilisation (one byte per window position). */
+#define DLLM_TOKEN_INVISIBLE 0  /* masked, or predicted with too little confidence: not context */
+#define DLLM_TOKEN_VISIBLE 1    /* exposed to later steps as context, still revisable */
+#define DLLM_TOKEN_STABLE 2     /* reliable enough for long-term reuse */
+
+/* Staged token stabilisation for one segment [seg_begin, seg_begin + seg_len) of
+ * the window (System Design, "Staged Token Stabilization"; the Evaluation setup
+ * uses theta_visible 0.7 and theta_stable 0.9), a variant of dllm_commit:
+ *   - every INVISIBLE position with conf >= theta_visible becomes VISIBLE: d_tok
+ *     takes its predicted id and its mask flag is cleared;
+ *   - if none does and INVISIBLE positions remain, the most confident of them
+ *     becomes VISIBLE (equal conf: the lower position), so decoding progresses;
+ *   - every VISIBLE position (just promoted or earlier) with conf >= theta_stable
+ *     becomes STABLE.  A VISIBLE position keeps its id: identity revision goes
+ *     through dllm_refresh_kv.
+ * d_state (device, one byte per window position) holds the states and is
+ * updated in place; positions outside the segment are untouched.  Comparisons
+ * are in fp32.  d_promoted_pos (nullable, >= seg_len entries) receives the
+ * positions that left INVISIBLE in ascending order, d_n_promoted (nullable) their
+ * count.  Requires 1 <= seg_len <= 1024, seg_begin >= 0 and finite thresholds;
+ * E_INVAL otherwise, before any launch.  Asynchronous on `stream`. */
+int dllm_commit_staged(const float* d_conf, const int32_t* d_id, int32_t* d_tok, uint8_t* d_mask,
+                       uint8_t* d_state, int32_t seg_begin, int32_t seg_len, float theta_visible,
+                       float theta_stable, int32_t* d_promoted_pos, int32_t* d_n_promoted, dllm_stream stream);
+
 /* Measurement helper: one launch of a plain streaming read over `bytes` bytes of
  * the device buffer d_buf (16-byte aligned; bytes a multiple of 16), the same
  * 16-byte-per-lane non-temporal loads the GEMMs stream weights with.  The caller

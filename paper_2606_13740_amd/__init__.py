@@ -69,6 +69,8 @@ _SIGNATURES = {
     "dllm_probe_read": ([_vp, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dllm_kernel_bytes": ([_vp, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dllm_read_bandwidth": ([_vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
+    "dllm_commit_staged": ([_vp, _vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_float, ctypes.c_float, _vp, _vp, _vp],
+                           ctypes.c_int),
 }
 
 
@@ -197,6 +199,16 @@ def dllm_kernel_bytes(model: int, kernel_class: int, W: int, P: int) -> float:
     b = ctypes.c_double()
     _check(lib().dllm_kernel_bytes(model, kernel_class, W, P, ctypes.byref(b)), "dllm_kernel_bytes")
     return b.value
+
+
+DLLM_TOKEN_INVISIBLE, DLLM_TOKEN_VISIBLE, DLLM_TOKEN_STABLE = 0, 1, 2
+
+
+def dllm_commit_staged(conf, ids, tok, mask, state, seg_begin: int, seg_len: int, theta_visible: float,
+                       theta_stable: float, promoted_pos=None, n_promoted=None, stream=None):
+    _check(lib().dllm_commit_staged(_ptr(conf), _ptr(ids), _ptr(tok), _ptr(mask), _ptr(state), seg_begin, seg_len,
+                                    theta_visible, theta_stable, _ptr(promoted_pos), _ptr(n_promoted),
+                                    _stream(stream)), "dllm_commit_staged")
 
 
 def dllm_read_bandwidth(buf, nbytes: int, sink, stream=None):

@@ -9,6 +9,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -819,6 +820,20 @@ int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int3
         default: return fail(DLLM_E_INVAL, "unknown kernel class");
     }
     *bytes = b;
+    return DLLM_OK;
+}
+
+int dllm_commit_staged(const float* d_conf, const int32_t* d_id, int32_t* d_tok, uint8_t* d_mask,
+                       uint8_t* d_state, int32_t seg_begin, int32_t seg_len, float theta_visible,
+                       float theta_stable, int32_t* d_promoted_pos, int32_t* d_n_promoted, dllm_stream stream) {
+    if (!d_conf || !d_id || !d_tok || !d_mask || !d_state) return fail(DLLM_E_INVAL, "NULL argument");
+    if (seg_begin < 0 || seg_len < 1 || seg_len > 1024) return fail(DLLM_E_INVAL, "segment must hold 1..1024 rows");
+    if (!std::isfinite(theta_visible) || !std::isfinite(theta_stable))
+        return fail(DLLM_E_INVAL, "thresholds must be finite");
+    hipLaunchKernelGGL(commit_staged_kernel, dim3(1), dim3(1024), 0, (hipStream_t)stream, d_conf, (const int*)d_id,
+                       (int*)d_tok, d_mask, d_state, seg_begin, seg_len, theta_visible, theta_stable,
+                       (int*)d_promoted_pos, (int*)d_n_promoted);
+    HIP_TRY(hipGetLastError());
     return DLLM_OK;
 }
 

@@ -213,6 +213,59 @@ commit_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, int seg
 }
 
 // ---------------------------------------------------------------------------
+// Staged token stabilisation over one segment (one thread per position, <= 1024):
+// state 0 invisible (masked), 1 visible, 2 stable.  Invisible positions at or
+// above tv become visible (taking their predicted id); if there is none, the
+// most confident invisible position does (ties: lower position); visible
+// positions at or above ts become stable.  The promoted positions are written
+// in ascending order.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(1024)
+commit_staged_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, uint8_t* state, int seg_begin,
+                     int seg_len, float tv, float ts, int* promoted, int* n_promoted) {
+    __shared__ unsigned long long best;
+    __shared__ int wsum[16];
+    const int i = threadIdx.x;
+    const bool in = i < seg_len;
+    const int p = seg_begin + i;
+    const uint8_t st = in ? state[p] : (uint8_t)2;
+    const float c = in ? conf[p] : 0.f;
+    const bool cand = in && st == 0;
+    if (i == 0) best = 0ull;
+    const bool vis = cand && c >= tv;
+    const int nvis = __syncthreads_count(vis);     // also orders the reset of `best`
+    bool prom = vis;
+    if (nvis == 0) {
+        // confidences are >= 0, so their bit patterns order like the values; the low
+        // word (>= 1) prefers the lower position and marks that a candidate exists
+        if (cand) atomicMax(&best, ((unsigned long long)__float_as_uint(c) << 32) | (unsigned)(1024 - i));
+        __syncthreads();
+        prom = cand && best != 0ull && (int)(1024u - (unsigned)(best & 0xFFFFFFFFull)) == i;
+    }
+    uint8_t ns = prom ? (uint8_t)1 : st;
+    if (ns == 1 && c >= ts) ns = 2;
+    if (in) {
+        if (prom) {
+            tok[p] = id[p];
+            mask[p] = 0;
+        }
+        if (ns != st) state[p] = ns;
+    }
+    const unsigned long long bal = __ballot(prom);
+    const int lane = i & 63, w = i >> 6;
+    if (lane == 0) wsum[w] = __popcll(bal);
+    __syncthreads();
+    int off = 0;
+    for (int j = 0; j < w; ++j) off += wsum[j];
+    if (prom && promoted != nullptr) promoted[off + __popcll(bal & ((1ull << lane) - 1ull))] = p;
+    if (i == 0 && n_promoted != nullptr) {
+        int t = 0;
+        for (int j = 0; j < (int)(blockDim.x >> 6); ++j) t += wsum[j];
+        *n_promoted = t;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Weight prepacking into MFMA chunks.  Packed row r takes source row
 // rowmap(r) of one of up to three source matrices (or zeros for padding).
 // ---------------------------------------------------------------------------

@@ -112,5 +112,17 @@ def test_read_bandwidth_validates_on_host(dl):
     assert L.dllm_read_bandwidth(ctypes.c_void_p(0x1000), 17, ctypes.c_void_p(0x2000), None) == dl.DLLM_E_INVAL
 
 
+@pytest.mark.parametrize("args,code", [
+    ((None, 1, 1, 1, 1, 0, 4, 0.7, 0.9), -1),          # null pointer
+    ((1, 1, 1, 1, 1, 0, 0, 0.7, 0.9), -1),             # empty segment
+    ((1, 1, 1, 1, 1, 0, 1025, 0.7, 0.9), -1),          # segment too long
+    ((1, 1, 1, 1, 1, -1, 4, 0.7, 0.9), -1),            # negative begin
+    ((1, 1, 1, 1, 1, 0, 4, float("nan"), 0.9), -1),    # non-finite threshold
+])
+def test_commit_staged_validates_on_host(dl, args, code):
+    rc = dl.lib().dllm_commit_staged(*args, None, None, None)
+    assert rc == code and dl.lib().dllm_last_error()
+
+
 def test_version_string(dl):
     assert dl.lib().dllm_version().startswith(b"dllm")
