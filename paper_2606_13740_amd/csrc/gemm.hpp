@@ -31,9 +31,12 @@ struct GemmArgs {
 
 // Epilogue interface:
 //   static constexpr int kSmem                      LDS bytes the epilogue keeps per row group
-//   void prologue(char* sm, int n0, int nrows, int m0, int mcols) const
-//       called by every thread at kernel start (e.g. to stage tables in sm while
-//       the weights stream)
+//   struct Pre                                      registers its prologue carries (may be empty)
+//   void fetch(Pre& p, int n0, int nrows, int m0, int mcols) const
+//       global loads of tables the epilogue needs, issued by every thread before the
+//       first weight loads
+//   void stage(const Pre& p, char* sm, int n0, int nrows, int m0, int mcols) const
+//       stores them to sm once the first weight loads are in flight
 //   void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int part, char* sm) const
 // Y is LDS [nrows][ldy] holding final outputs of weight rows [n0, n0 + nrows) for
 // tokens [m0, m0 + mcols) (int8 row scales applied); every thread of the
@@ -84,16 +87,27 @@ gemm_kernel(GemmArgs g, Epi epi) {
     const int wave = threadIdx.x >> 6;
     const int wn = wave % NWn, wk = wave / NWn;
     const int mt0 = blockIdx.z * MT;
-    const int KS = gridDim.y;
-    const int kb0 = (int)(((long)blockIdx.y * g.KCw) / KS);
-    const int kb1 = (int)(((long)(blockIdx.y + 1) * g.KCw) / KS);
+    // K range of this split (32-bit unsigned: KCw * KS is far below 2^32, and a 64-bit
+    // division would delay the first weight load by a few hundred scalar instructions)
+    const unsigned KS = gridDim.y, KCw = (unsigned)g.KCw;
+    const int kb0 = KS == 1 ? 0 : (int)((blockIdx.y * KCw) / KS);
+    const int kb1 = KS == 1 ? g.KCw : (int)(((blockIdx.y + 1) * KCw) / KS);
 
+    typename Epi::Pre pre[NWn];
 #pragma unroll
     for (int q = 0; q < NWn; ++q) {
         const int nq0 = (blockIdx.x * NWn + q) * FW;
         const int nfq = max(0, min(FW, g.n_tiles - nq0));
-        if (nfq > 0) epi.prologue(esm + q * ESM, nq0 * 16, nfq * 16, mt0 * 16, MR);
+        if (nfq > 0) epi.fetch(pre[q], nq0 * 16, nfq * 16, mt0 * 16, MR);
     }
+    auto stage_prologue = [&]() {
+#pragma unroll
+        for (int q = 0; q < NWn; ++q) {
+            const int nq0 = (blockIdx.x * NWn + q) * FW;
+            const int nfq = max(0, min(FW, g.n_tiles - nq0));
+            if (nfq > 0) epi.stage(pre[q], esm + q * ESM, nq0 * 16, nfq * 16, mt0 * 16, MR);
+        }
+    };
 
     f32x4_t acc[FW][MT];
 #pragma unroll
@@ -104,8 +118,9 @@ gemm_kernel(GemmArgs g, Epi epi) {
     {
         const int nt0 = (blockIdx.x * NWn + wn) * FW;
         const int nf = max(0, min(FW, g.n_tiles - nt0));
-        const int c0 = kb0 + (int)(((long)wk * (kb1 - kb0)) / NWk);
-        const int c1 = kb0 + (int)(((long)(wk + 1) * (kb1 - kb0)) / NWk);
+        const unsigned span = (unsigned)(kb1 - kb0);
+        const int c0 = kb0 + (int)(((unsigned)wk * span) / NWk);
+        const int c1 = kb0 + (int)(((unsigned)(wk + 1) * span) / NWk);
         const char* wp = (const char*)g.W + ((size_t)nt0 * g.KCw * 64 + lane) * 16;
         const char* xp = (const char*)g.X + (size_t)mt0 * g.KCx * XB + lane * 16;
         const size_t wtile = (size_t)g.KCw * 1024, xtile = (size_t)g.KCx * XB;
@@ -157,9 +172,13 @@ gemm_kernel(GemmArgs g, Epi epi) {
             }
         };
 
-        if (c1 > c0 && nf > 0) {
+        const bool work = c1 > c0 && nf > 0;
+        if (work) {
 #pragma unroll
             for (int s = 0; s < D; ++s) load(s, min(c0 + s, c1 - 1));
+        }
+        stage_prologue();
+        if (work) {
             for (int base = c0; base < c1; base += D) {
 #pragma unroll
                 for (int s = 0; s < D; ++s) {
@@ -257,18 +276,44 @@ struct EpiQKV {
         }
     }
 
-    // (cos, sin) of every (pair, token) of the group's Q/K rows, fetched while the weights stream
-    __device__ void prologue(char* sm, int n0, int nrows, int m0, int mcols) const {
-        const int npairs = nrows >> 1;
-        if (npairs * mcols > kPairs) return;
+    // (cos, sin) of every (pair, token) of the group's Q/K rows: the first kPre per
+    // thread go through registers (loaded before the weights), the rest (only for
+    // workgroups of fewer than kPairs / kPre threads) are copied directly in stage()
+    static constexpr int kPre = 3;
+    struct Pre {
+        float2 cs[kPre];
+    };
+    __device__ __forceinline__ bool rope_entry(int idx, int n0, int npairs, int m0, float2& v) const {
+        const int p = idx % npairs, ml = idx / npairs;
+        const int m = m0 + ml, n = n0 + 2 * p;
+        if (m >= M || n >= 2 * d) return false;
+        const int rr = (n % d) % Dh;
+        const int ps = pos ? pos[m] : pos_base + m;
+        v = rope[(size_t)ps * (Dh >> 1) + (rr >> 1)];
+        return true;
+    }
+    __device__ void fetch(Pre& pr, int n0, int nrows, int m0, int mcols) const {
+        const int npairs = nrows >> 1, n = npairs * mcols;
+        if (n > kPairs) return;
+#pragma unroll
+        for (int u = 0; u < kPre; ++u) {
+            const int idx = threadIdx.x + u * blockDim.x;
+            pr.cs[u] = make_float2(0.f, 0.f);
+            if (idx < n) rope_entry(idx, n0, npairs, m0, pr.cs[u]);
+        }
+    }
+    __device__ void stage(const Pre& pr, char* sm, int n0, int nrows, int m0, int mcols) const {
+        const int npairs = nrows >> 1, n = npairs * mcols;
+        if (n > kPairs) return;
         float2* cs = (float2*)sm;
-        for (int idx = threadIdx.x; idx < npairs * mcols; idx += blockDim.x) {
-            const int p = idx % npairs, ml = idx / npairs;
-            const int m = m0 + ml, n = n0 + 2 * p;
-            if (m >= M || n >= 2 * d) continue;
-            const int rr = (n % d) % Dh;
-            const int ps = pos ? pos[m] : pos_base + m;
-            cs[idx] = rope[(size_t)ps * (Dh >> 1) + (rr >> 1)];
+#pragma unroll
+        for (int u = 0; u < kPre; ++u) {
+            const int idx = threadIdx.x + u * blockDim.x;
+            if (idx < n) cs[idx] = pr.cs[u];
+        }
+        for (int idx = threadIdx.x + kPre * blockDim.x; idx < n; idx += blockDim.x) {
+            float2 v;
+            if (rope_entry(idx, n0, npairs, m0, v)) cs[idx] = v;
         }
     }
 
@@ -377,7 +422,9 @@ struct EpiPartial {
     int rows;               // token rows per K slice of P
 
     static constexpr int kSmem = 0;
-    __device__ void prologue(char*, int, int, int, int) const {}
+    struct Pre {};
+    __device__ void fetch(Pre&, int, int, int, int) const {}
+    __device__ void stage(const Pre&, char*, int, int, int, int) const {}
 
     __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int, char*) const {
         float* base = P + (size_t)blockIdx.y * rows * ldn;
@@ -398,7 +445,9 @@ struct EpiSwiGLU {
     int KCx;
 
     static constexpr int kSmem = 0;
-    __device__ void prologue(char*, int, int, int, int) const {}
+    struct Pre {};
+    __device__ void fetch(Pre&, int, int, int, int) const {}
+    __device__ void stage(const Pre&, char*, int, int, int, int) const {}
 
     // four consecutive outputs (eight packed rows) per thread
     __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int, char*) const {
@@ -441,7 +490,9 @@ struct EpiLM {
     float* logits;          // [M][V] or nullptr
 
     static constexpr int kSmem = 0;
-    __device__ void prologue(char*, int, int, int, int) const {}
+    struct Pre {};
+    __device__ void fetch(Pre&, int, int, int, int) const {}
+    __device__ void stage(const Pre&, char*, int, int, int, int) const {}
 
     // TPT consecutive lanes per token, each an online (max, argmax, sum exp) over a
     // slice of the rows, then a fixed shuffle tree over the slices.
