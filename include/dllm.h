@@ -201,6 +201,32 @@ int dllm_append_prefix_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_block_tok
 int dllm_refresh_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_pos, const int32_t* d_new_id,
                     int32_t n, int32_t* d_out_id, float* d_out_conf, dllm_stream stream);
 
+/* Piggybacked append and refresh: one forward over three row groups that is, row
+ * for row, the sequence dllm_refresh_kv(ref) -> dllm_append_prefix_kv(block) ->
+ * dllm_denoise_step(window) (System Design, "Sparse Cache Refresh": revisions are
+ * merged at step boundaries; "Multi-Block Speculative Decoding": a completed
+ * block becomes prefix before the next step), streaming the weights once instead
+ * of three times:
+ *   - rows [0, n_ref): revised prefix positions d_ref_pos[i] with ids d_ref_id[i]
+ *     (as dllm_refresh_kv: keys up to the end of their block, capped at P, the
+ *     prefix length on entry; their new K/V replace the cached ones layer by
+ *     layer);
+ *   - rows [n_ref, n_ref + n_block): the completed block d_block_tok (no MASK) at
+ *     positions P.., keys [0, P + n_block), written into the prefix;
+ *   - the last W rows: the window d_tok / d_mask (nullable) at positions
+ *     P + n_block.., keys [0, P + n_block + W), as dllm_denoise_step.
+ * A refresh position inside the block being appended is expressed by appending
+ * the block with the revised id.  Outputs (each pair both set or both NULL):
+ * d_out_id / d_out_conf [W] for the window, d_ref_out_id / d_ref_out_conf [n_ref]
+ * for the refresh rows.  prefix_len becomes P + n_block.  Any group may be empty;
+ * E_INVAL unless 1 <= n_ref + n_block + W <= max_window and the refresh positions
+ * are distinct and < P (they are copied to the host, so the call synchronises
+ * `stream` when n_ref > 0); E_CAPACITY if P + n_block + W > capacity. */
+int dllm_step_merged(dllm_model* m, dllm_kv* kv, const int32_t* d_ref_pos, const int32_t* d_ref_id,
+                     int32_t n_ref, const int32_t* d_block_tok, int32_t n_block, const int32_t* d_tok,
+                     const uint8_t* d_mask, int32_t W, int32_t* d_out_id, float* d_out_conf,
+                     int32_t* d_ref_out_id, float* d_ref_out_conf, dllm_stream stream);
+
 /* Parity only (never on the timed path): the same step as dllm_denoise_step, also
  * writing the full logits d_logits[W][vocab] (float, MASK column = -inf).  If
  * d_out_id / d_out_conf are non-NULL they receive the step's outputs. */

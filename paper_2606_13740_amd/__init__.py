@@ -63,6 +63,8 @@ _SIGNATURES = {
     "dllm_commit": ([_vp, _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_append_prefix_kv": ([_vp, _vp, _vp, _i32, _vp], ctypes.c_int),
     "dllm_refresh_kv": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_step_merged": ([_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp],
+                         ctypes.c_int),
     "dllm_debug_logits": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp], ctypes.c_int),
     "dllm_debug_hidden": ([_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp], ctypes.c_int),
     "dllm_probe_enable": ([_vp, _i32, _i32], ctypes.c_int),
@@ -173,6 +175,13 @@ def dllm_append_prefix_kv(model: int, kv: int, block_tok, n: int, stream=None):
 def dllm_refresh_kv(model: int, kv: int, pos, new_ids, n: int, out_id=None, out_conf=None, stream=None):
     _check(lib().dllm_refresh_kv(model, kv, _ptr(pos), _ptr(new_ids), n, _ptr(out_id), _ptr(out_conf),
                                  _stream(stream)), "dllm_refresh_kv")
+
+
+def dllm_step_merged(model: int, kv: int, ref_pos, ref_ids, n_ref: int, block_tok, n_block: int, tok, mask,
+                     W: int, out_id=None, out_conf=None, ref_out_id=None, ref_out_conf=None, stream=None):
+    _check(lib().dllm_step_merged(model, kv, _ptr(ref_pos), _ptr(ref_ids), n_ref, _ptr(block_tok), n_block,
+                                  _ptr(tok), _ptr(mask), W, _ptr(out_id), _ptr(out_conf), _ptr(ref_out_id),
+                                  _ptr(ref_out_conf), _stream(stream)), "dllm_step_merged")
 
 
 def dllm_debug_logits(model: int, kv: int, tok, mask, W: int, logits, out_id=None, out_conf=None, stream=None):

@@ -75,6 +75,10 @@ struct Workspace {
     float* opart = nullptr;  // [MAX_SPLIT][wrows][H][Dh]
     float* mlpart = nullptr; // [MAX_SPLIT][wrows][H][2]
     size_t xg_bytes = 0, of_bytes = 0, af_bytes = 0;   // allocated fragment-buffer sizes
+    int* tok = nullptr;      // [rows] ids of a merged pass
+    uint8_t* msk = nullptr;  // [rows] mask flags of a merged pass
+    int* oid = nullptr;      // [rows] argmax ids of a merged pass
+    float* oconf = nullptr;  // [rows] confidences of a merged pass
 };
 
 constexpr int MAX_SPLIT = 16;
@@ -215,7 +219,7 @@ struct ProbeScope {
 // ---------------------------------------------------------------------------
 
 void free_ws(Workspace& w) {
-    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart};
+    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart, w.tok, w.msk, w.oid, w.oconf};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     w = Workspace{};
@@ -258,6 +262,10 @@ int ensure_ws(dllm_model* m, int rows_needed) {
     ALLOC(w.part, w.part_floats * 4);
     ALLOC(w.opart, (size_t)MAX_SPLIT * w.wrows * d * 4);
     ALLOC(w.mlpart, (size_t)MAX_SPLIT * w.wrows * c.n_heads * 2 * 4);
+    ALLOC(w.tok, (size_t)rows * 4);
+    ALLOC(w.msk, (size_t)rows);
+    ALLOC(w.oid, (size_t)rows * 4);
+    ALLOC(w.oconf, (size_t)rows * 4);
 #undef ALLOC
     return DLLM_OK;
 }
@@ -768,6 +776,51 @@ int dllm_refresh_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_pos, const int3
     a.M = n; a.tok = d_new_id; a.pos = m->ws.pos; a.T = T; a.lim = m->ws.lim;
     a.n_layers = m->cfg.n_layers; a.lm = d_out_id != nullptr; a.out_id = d_out_id; a.out_conf = d_out_conf;
     return forward(m, kv, a, s);
+}
+
+int dllm_step_merged(dllm_model* m, dllm_kv* kv, const int32_t* d_ref_pos, const int32_t* d_ref_id, int32_t n_ref,
+                     const int32_t* d_block_tok, int32_t n_block, const int32_t* d_tok, const uint8_t* d_mask,
+                     int32_t W, int32_t* d_out_id, float* d_out_conf, int32_t* d_ref_out_id, float* d_ref_out_conf,
+                     dllm_stream stream) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (n_ref < 0 || n_block < 0 || W < 0) return fail(DLLM_E_INVAL, "row counts must be >= 0");
+    const int M = n_ref + n_block + W;
+    if (M < 1 || M > m->cfg.max_window) return fail(DLLM_E_INVAL, "n_ref + n_block + W must be in [1, max_window]");
+    if ((n_ref > 0 && (!d_ref_pos || !d_ref_id)) || (n_block > 0 && !d_block_tok) || (W > 0 && !d_tok))
+        return fail(DLLM_E_INVAL, "NULL input pointer for a non-empty row group");
+    if ((d_out_id == nullptr) != (d_out_conf == nullptr) || (d_ref_out_id == nullptr) != (d_ref_out_conf == nullptr))
+        return fail(DLLM_E_INVAL, "each id / conf output pair must be both set or both NULL");
+    const int P = kv->prefix_len;
+    if (P + n_block + W > kv->capacity) return fail(DLLM_E_CAPACITY, "prefix_len + n_block + W exceeds the capacity");
+    hipStream_t s = (hipStream_t)stream;
+    if (n_ref > 0) {
+        std::vector<int32_t> pos(n_ref);
+        HIP_TRY(hipMemcpyAsync(pos.data(), d_ref_pos, (size_t)n_ref * 4, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        std::sort(pos.begin(), pos.end());
+        for (int i = 0; i < n_ref; ++i) {
+            if (pos[i] < 0 || pos[i] >= P) return fail(DLLM_E_INVAL, "refresh position outside [0, prefix_len)");
+            if (i > 0 && pos[i] == pos[i - 1]) return fail(DLLM_E_INVAL, "refresh positions must be distinct");
+        }
+    }
+    if ((rc = ensure_ws(m, M))) return rc;
+    Workspace& w = m->ws;
+    hipLaunchKernelGGL(merged_rows_kernel, dim3(ceil_div(M, 64)), dim3(64), 0, s, d_ref_pos, d_ref_id, n_ref,
+                       d_block_tok, n_block, d_tok, d_mask, W, P, kv->prompt_len, m->cfg.block, w.tok, w.msk, w.pos,
+                       w.lim);
+    const bool lm = (d_out_id != nullptr && W > 0) || (d_ref_out_id != nullptr && n_ref > 0);
+    FwdArgs a{};
+    a.M = M; a.tok = w.tok; a.mask = w.msk; a.pos = w.pos; a.T = P + n_block + W; a.lim = w.lim;
+    a.n_layers = m->cfg.n_layers; a.lm = lm; a.out_id = w.oid; a.out_conf = w.oconf;
+    if ((rc = forward(m, kv, a, s))) return rc;
+    if (lm) {
+        hipLaunchKernelGGL(merged_out_kernel, dim3(ceil_div(M, 64)), dim3(64), 0, s, (const int*)w.oid,
+                           (const float*)w.oconf, n_ref, n_block, W, d_ref_out_id, d_ref_out_conf, d_out_id, d_out_conf);
+        HIP_TRY(hipGetLastError());
+    }
+    kv->prefix_len = P + n_block;
+    return DLLM_OK;
 }
 
 int dllm_probe_enable(dllm_model* m, int32_t kernel_class, int32_t max_records) {

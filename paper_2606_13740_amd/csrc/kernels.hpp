@@ -392,4 +392,51 @@ __global__ void refresh_limits_kernel(const int* pos, int n, int prompt_len, int
     lim[i] = min(e, prefix_len);
 }
 
+// Rows of a merged pass (refresh, append and step in one forward): rows [0, n_ref)
+// are revised prefix positions (keys up to the end of their block, capped at P),
+// rows [n_ref, n_ref + n_blk) the completed block at P.. (keys [0, P + n_blk)),
+// the last W rows the window at P + n_blk.. (keys [0, P + n_blk + W), mask kept).
+__global__ void merged_rows_kernel(const int* ref_pos, const int* ref_id, int n_ref, const int* blk, int n_blk,
+                                   const int* tok, const uint8_t* mask, int W, int P, int prompt_len, int block,
+                                   int* otok, uint8_t* omask, int* opos, int* olim) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_ref + n_blk + W) return;
+    int t, p, l;
+    uint8_t mk = 0;
+    if (i < n_ref) {
+        p = ref_pos[i];
+        t = ref_id[i];
+        const int e = (p < prompt_len) ? prompt_len : prompt_len + block * (1 + (p - prompt_len) / block);
+        l = min(e, P);
+    } else if (i < n_ref + n_blk) {
+        const int j = i - n_ref;
+        t = blk[j];
+        p = P + j;
+        l = P + n_blk;
+    } else {
+        const int j = i - n_ref - n_blk;
+        t = tok[j];
+        mk = mask ? mask[j] : (uint8_t)0;
+        p = P + n_blk + j;
+        l = P + n_blk + W;
+    }
+    otok[i] = t;
+    omask[i] = mk;
+    opos[i] = p;
+    olim[i] = l;
+}
+
+// Outputs of a merged pass: the refresh rows' and the window rows' (id, conf).
+__global__ void merged_out_kernel(const int* oid, const float* oconf, int n_ref, int n_blk, int W, int* ref_id,
+                                  float* ref_conf, int* out_id, float* out_conf) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n_ref && ref_id) {
+        ref_id[i] = oid[i];
+        ref_conf[i] = oconf[i];
+    } else if (i >= n_ref + n_blk && i < n_ref + n_blk + W && out_id) {
+        out_id[i - n_ref - n_blk] = oid[i];
+        out_conf[i - n_ref - n_blk] = oconf[i];
+    }
+}
+
 }  // namespace dllm

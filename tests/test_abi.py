@@ -98,6 +98,8 @@ def test_null_handles_are_rejected(dl):
     assert L.dllm_denoise_step(None, None, None, None, 32, None, None, None) == dl.DLLM_E_INVAL
     assert L.dllm_append_prefix_kv(None, None, None, 32, None) == dl.DLLM_E_INVAL
     assert L.dllm_refresh_kv(None, None, None, None, 4, None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_step_merged(None, None, None, None, 0, None, 32, None, None, 0, None, None, None, None,
+                              None) == dl.DLLM_E_INVAL
     assert L.dllm_prefill(None, None, None, 4, None) == dl.DLLM_E_INVAL
     assert L.dllm_kv_set_prefix_len(None, 0) == dl.DLLM_E_INVAL
     assert L.dllm_model_destroy(None) == dl.DLLM_OK
