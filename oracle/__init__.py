@@ -5,6 +5,7 @@ benchmark's CPU-baseline leg.  The product path never imports it.
 """
 from .model import (  # noqa: F401
     IV, S, V, OracleKV, OracleModel, StepOut, append_block, attend, attend_masked, block_causal_allowed,
-    commit, commit_schedule, commit_staged, confidence, denoise_step, dequantize_rows, forward_full,
+    commit, commit_schedule, commit_staged, confidence, denoise_step, denoise_window, dequantize_rows, forward_full,
     forward_rows, input_ids, prefill, quantize_rows_int8, refresh, rmsnorm, rope, silu, softmax,
 )
+from . import mbsd  # noqa: F401,E402

@@ -332,6 +332,22 @@ def denoise_step(model: OracleModel, kv: OracleKV, tok: np.ndarray, mask: np.nda
     return StepOut(logits, ids_out, conf, x)
 
 
+def denoise_window(model: OracleModel, kv: OracleKV, w0: int, tok: np.ndarray, mask: np.ndarray) -> StepOut:
+    """One denoising step over a decoding window at [w0, w0 + W) with w0 >= P
+    (System Design, "Multi-Block Speculative Decoding": the window is the execution
+    unit and slides along the commit frontier).  Rows [P, w0) are committed
+    positions the window has slid past: their cached K/V are the ones an earlier
+    window step wrote and are reused as they are.  Window rows attend to every key in
+    [0, w0 + W); their K/V land in rows [w0, w0 + W).  With w0 = P this is
+    denoise_step."""
+    W = len(tok)
+    assert kv.prefix_len <= w0 and w0 + W <= kv.capacity
+    ids = input_ids(model.shape, tok, mask)
+    x, logits = forward_rows(model, kv, ids, w0 + np.arange(W), np.full(W, w0 + W), lm_head=True)
+    ids_out, conf = confidence(logits)
+    return StepOut(logits, ids_out, conf, x)
+
+
 def commit(conf: np.ndarray, pred: np.ndarray, tok: np.ndarray, mask: np.ndarray,
            seg_begin: int, seg_len: int, k: int):
     """Commit the k most confident masked positions of [seg_begin, seg_begin + seg_len).
