@@ -227,6 +227,19 @@ int dllm_step_merged(dllm_model* m, dllm_kv* kv, const int32_t* d_ref_pos, const
                      const uint8_t* d_mask, int32_t W, int32_t* d_out_id, float* d_out_conf,
                      int32_t* d_ref_out_id, float* d_ref_out_conf, dllm_stream stream);
 
+/* A denoising step over a decoding window that has slid past committed positions
+ * (System Design, "Multi-Block Speculative Decoding": the window, not the block,
+ * is the execution unit and moves with the commit frontier).  The W rows sit at
+ * positions [w0, w0 + W) with w0 >= prefix_len and attend to every key in
+ * [0, w0 + W); rows [prefix_len, w0) are positions an earlier window step wrote
+ * and are reused as they are (the caller keeps them current).  Their K/V land in
+ * rows [w0, w0 + W).  Outputs as dllm_denoise_step; prefix_len is unchanged.
+ * With w0 = prefix_len this is dllm_denoise_step.  E_INVAL if W is not in
+ * [1, max_window] or w0 < prefix_len; E_CAPACITY if w0 + W > capacity. */
+int dllm_denoise_window(dllm_model* m, dllm_kv* kv, int32_t w0, const int32_t* d_tok,
+                        const uint8_t* d_mask, int32_t W, int32_t* d_out_id, float* d_out_conf,
+                        dllm_stream stream);
+
 /* Parity only (never on the timed path): the same step as dllm_denoise_step, also
  * writing the full logits d_logits[W][vocab] (float, MASK column = -inf).  If
  * d_out_id / d_out_conf are non-NULL they receive the step's outputs. */
@@ -284,6 +297,23 @@ int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int3
 int dllm_commit_staged(const float* d_conf, const int32_t* d_id, int32_t* d_tok, uint8_t* d_mask,
                        uint8_t* d_state, int32_t seg_begin, int32_t seg_len, float theta_visible,
                        float theta_stable, int32_t* d_promoted_pos, int32_t* d_n_promoted, dllm_stream stream);
+
+/* Draft acceptance (System Design, "Multi-Block Speculative Decoding": when a
+ * future block becomes current its draft tokens are re-evaluated and accepted only
+ * if they meet the commitment criterion).  Over n position-aligned entries: every
+ * position with d_mask = 1, d_draft_id >= 0, d_id == d_draft_id and
+ * d_conf >= theta (fp32) is committed (d_tok = d_id, d_mask = 0).
+ * d_accepted_pos (nullable, >= n entries) receives the accepted indices in
+ * ascending order, d_n_accepted (nullable) their count.  E_INVAL unless
+ * 1 <= n <= 1024 and theta is finite, before any launch. */
+int dllm_accept_drafts(const float* d_conf, const int32_t* d_id, const int32_t* d_draft_id,
+                       int32_t* d_tok, uint8_t* d_mask, int32_t n, float theta,
+                       int32_t* d_accepted_pos, int32_t* d_n_accepted, dllm_stream stream);
+
+/* Draft records for window rows past the current block: d_draft_id[i] = d_id[i]
+ * where d_mask[i] = 1, else -1, for n position-aligned entries (n >= 1). */
+int dllm_record_drafts(const int32_t* d_id, const uint8_t* d_mask, int32_t* d_draft_id, int32_t n,
+                       dllm_stream stream);
 
 /* Measurement helper: one launch of a plain streaming read over `bytes` bytes of
  * the device buffer d_buf (16-byte aligned; bytes a multiple of 16), the same

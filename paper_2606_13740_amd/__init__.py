@@ -63,6 +63,9 @@ _SIGNATURES = {
     "dllm_commit": ([_vp, _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_append_prefix_kv": ([_vp, _vp, _vp, _i32, _vp], ctypes.c_int),
     "dllm_refresh_kv": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_denoise_window": ([_vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_accept_drafts": ([_vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_record_drafts": ([_vp, _vp, _vp, _i32, _vp], ctypes.c_int),
     "dllm_step_merged": ([_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp],
                          ctypes.c_int),
     "dllm_debug_logits": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp], ctypes.c_int),
@@ -175,6 +178,22 @@ def dllm_append_prefix_kv(model: int, kv: int, block_tok, n: int, stream=None):
 def dllm_refresh_kv(model: int, kv: int, pos, new_ids, n: int, out_id=None, out_conf=None, stream=None):
     _check(lib().dllm_refresh_kv(model, kv, _ptr(pos), _ptr(new_ids), n, _ptr(out_id), _ptr(out_conf),
                                  _stream(stream)), "dllm_refresh_kv")
+
+
+def dllm_denoise_window(model: int, kv: int, w0: int, tok, mask, W: int, out_id, out_conf, stream=None):
+    _check(lib().dllm_denoise_window(model, kv, w0, _ptr(tok), _ptr(mask), W, _ptr(out_id), _ptr(out_conf),
+                                     _stream(stream)), "dllm_denoise_window")
+
+
+def dllm_accept_drafts(conf, ids, draft_ids, tok, mask, n: int, theta: float, accepted_pos=None, n_accepted=None,
+                       stream=None):
+    _check(lib().dllm_accept_drafts(_ptr(conf), _ptr(ids), _ptr(draft_ids), _ptr(tok), _ptr(mask), n, float(theta),
+                                    _ptr(accepted_pos), _ptr(n_accepted), _stream(stream)), "dllm_accept_drafts")
+
+
+def dllm_record_drafts(ids, mask, draft_ids, n: int, stream=None):
+    _check(lib().dllm_record_drafts(_ptr(ids), _ptr(mask), _ptr(draft_ids), n, _stream(stream)),
+           "dllm_record_drafts")
 
 
 def dllm_step_merged(model: int, kv: int, ref_pos, ref_ids, n_ref: int, block_tok, n_block: int, tok, mask,

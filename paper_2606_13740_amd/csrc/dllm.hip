@@ -698,6 +698,20 @@ int dllm_denoise_step(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const ui
     return forward(m, kv, a, (hipStream_t)stream);
 }
 
+int dllm_denoise_window(dllm_model* m, dllm_kv* kv, int32_t w0, const int32_t* d_tok, const uint8_t* d_mask,
+                        int32_t W, int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (!d_tok || !d_out_id || !d_out_conf) return fail(DLLM_E_INVAL, "NULL argument");
+    if (W < 1 || W > m->cfg.max_window) return fail(DLLM_E_INVAL, "W must be in [1, max_window]");
+    if (w0 < kv->prefix_len) return fail(DLLM_E_INVAL, "w0 must be >= prefix_len");
+    if ((long)w0 + W > kv->capacity) return fail(DLLM_E_CAPACITY, "w0 + W exceeds the cache capacity");
+    FwdArgs a{};
+    a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = w0; a.T = w0 + W;
+    a.n_layers = m->cfg.n_layers; a.lm = true; a.out_id = d_out_id; a.out_conf = d_out_conf;
+    return forward(m, kv, a, (hipStream_t)stream);
+}
+
 int dllm_debug_logits(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
                       float* d_logits, int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
     int rc = window_checks(m, kv, d_tok, W);
@@ -886,6 +900,29 @@ int dllm_commit_staged(const float* d_conf, const int32_t* d_id, int32_t* d_tok,
     hipLaunchKernelGGL(commit_staged_kernel, dim3(1), dim3(1024), 0, (hipStream_t)stream, d_conf, (const int*)d_id,
                        (int*)d_tok, d_mask, d_state, seg_begin, seg_len, theta_visible, theta_stable,
                        (int*)d_promoted_pos, (int*)d_n_promoted);
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
+int dllm_accept_drafts(const float* d_conf, const int32_t* d_id, const int32_t* d_draft_id, int32_t* d_tok,
+                       uint8_t* d_mask, int32_t n, float theta, int32_t* d_accepted_pos, int32_t* d_n_accepted,
+                       dllm_stream stream) {
+    if (!d_conf || !d_id || !d_draft_id || !d_tok || !d_mask) return fail(DLLM_E_INVAL, "NULL argument");
+    if (n < 1 || n > 1024) return fail(DLLM_E_INVAL, "n must be in [1, 1024]");
+    if (!std::isfinite(theta)) return fail(DLLM_E_INVAL, "theta must be finite");
+    hipLaunchKernelGGL(accept_drafts_kernel, dim3(1), dim3(1024), 0, (hipStream_t)stream, d_conf, (const int*)d_id,
+                       (const int*)d_draft_id, (int*)d_tok, d_mask, n, theta, (int*)d_accepted_pos,
+                       (int*)d_n_accepted);
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
+int dllm_record_drafts(const int32_t* d_id, const uint8_t* d_mask, int32_t* d_draft_id, int32_t n,
+                       dllm_stream stream) {
+    if (!d_id || !d_mask || !d_draft_id) return fail(DLLM_E_INVAL, "NULL argument");
+    if (n < 1) return fail(DLLM_E_INVAL, "n must be >= 1");
+    hipLaunchKernelGGL(record_drafts_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, (hipStream_t)stream,
+                       (const int*)d_id, d_mask, (int*)d_draft_id, n);
     HIP_TRY(hipGetLastError());
     return DLLM_OK;
 }

@@ -392,6 +392,43 @@ __global__ void refresh_limits_kernel(const int* pos, int n, int prompt_len, int
     lim[i] = min(e, prefix_len);
 }
 
+// Draft acceptance when a block becomes current: a masked position whose draft
+// record equals this step's prediction with conf >= theta is committed; the
+// accepted positions are written in ascending order (ballot compaction).
+__global__ void __launch_bounds__(1024)
+accept_drafts_kernel(const float* conf, const int* id, const int* draft, int* tok, uint8_t* mask, int n, float theta,
+                     int* accepted, int* n_accepted) {
+    __shared__ int wsum[16];
+    const int i = threadIdx.x;
+    bool a = false;
+    if (i < n && mask[i] == 1) {
+        const int dv = draft[i];
+        a = dv >= 0 && id[i] == dv && conf[i] >= theta;
+    }
+    if (a) {
+        tok[i] = id[i];
+        mask[i] = 0;
+    }
+    const unsigned long long bal = __ballot(a);
+    const int lane = i & 63, w = i >> 6;
+    if (lane == 0) wsum[w] = __popcll(bal);
+    __syncthreads();
+    int off = 0;
+    for (int j = 0; j < w; ++j) off += wsum[j];
+    if (a && accepted != nullptr) accepted[off + __popcll(bal & ((1ull << lane) - 1ull))] = i;
+    if (i == 0 && n_accepted != nullptr) {
+        int t = 0;
+        for (int j = 0; j < (int)(blockDim.x >> 6); ++j) t += wsum[j];
+        *n_accepted = t;
+    }
+}
+
+// Draft records: this step's prediction for masked positions, -1 elsewhere.
+__global__ void record_drafts_kernel(const int* id, const uint8_t* mask, int* draft, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) draft[i] = mask[i] == 1 ? id[i] : -1;
+}
+
 // Rows of a merged pass (refresh, append and step in one forward): rows [0, n_ref)
 // are revised prefix positions (keys up to the end of their block, capped at P),
 // rows [n_ref, n_ref + n_blk) the completed block at P.. (keys [0, P + n_blk)),

@@ -100,6 +100,19 @@ def test_null_handles_are_rejected(dl):
     assert L.dllm_refresh_kv(None, None, None, None, 4, None, None, None) == dl.DLLM_E_INVAL
     assert L.dllm_step_merged(None, None, None, None, 0, None, 32, None, None, 0, None, None, None, None,
                               None) == dl.DLLM_E_INVAL
+    assert L.dllm_denoise_window(None, None, 0, None, None, 32, None, None, None) == dl.DLLM_E_INVAL
+
+
+def test_draft_calls_validate_on_host(dl):
+    L = dl.lib()
+    buf = (ctypes.c_int32 * 8)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    assert L.dllm_accept_drafts(None, p, p, p, p, 4, ctypes.c_float(0.5), None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_accept_drafts(p, p, p, p, p, 0, ctypes.c_float(0.5), None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_accept_drafts(p, p, p, p, p, 1025, ctypes.c_float(0.5), None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_accept_drafts(p, p, p, p, p, 4, ctypes.c_float(float("nan")), None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_record_drafts(p, None, p, 4, None) == dl.DLLM_E_INVAL
+    assert L.dllm_record_drafts(p, p, p, 0, None) == dl.DLLM_E_INVAL
     assert L.dllm_prefill(None, None, None, 4, None) == dl.DLLM_E_INVAL
     assert L.dllm_kv_set_prefix_len(None, 0) == dl.DLLM_E_INVAL
     assert L.dllm_model_destroy(None) == dl.DLLM_OK
