@@ -39,6 +39,7 @@ DEFAULT = "llada8b_bf16_p512_w32"
 E2E = "llada8b_bf16_e2e128"      # end-to-end 128-token generation (prefill included)
 E2E_STAGED = "llada8b_bf16_e2e128_staged"   # the same with staged token stabilisation
 E2E_MERGED = "llada8b_bf16_e2e128_merged"   # the same with append + refresh piggybacked on the next step
+E2E_MBSD = "llada8b_bf16_e2e128_mbsd"       # the same with multi-block speculative decoding
 
 
 def run_e2e(args, dl, torch, shape, dev):
@@ -237,10 +238,89 @@ def run_e2e_staged(args, dl, torch, shape, dev):
     }
 
 
+def run_e2e_mbsd(args, dl, torch, shape, dev):
+    """Prompt 512 ids; 128 tokens (4 blocks of 32) decoded with multi-block
+    speculative decoding: a 32-row window slides along the commit frontier, one
+    commit per step, the window grows by the latency table once at most 4 masked
+    positions remain in the current block (allowance 10%), draft rows past the
+    current block are recorded and accepted when their block becomes current.  The
+    latency table is measured first: dllm_denoise_window at each row count.  Run
+    twice: acceptance threshold 0.9 (random weights give confidences near 1e-3, so
+    nothing is accepted: the mechanism's cost) and 0 (a draft is accepted whenever
+    the current step predicts the id it recorded)."""
+    from paper_2606_13740_amd.mbsd import MBSDGenerator
+
+    P0, B, NB, WN = 512, shape.block, 4, 32
+    rows = (32, 48, 64)
+    glob = synth.global_weights(shape, "bf16")
+    model = dl.Model(shape, "bf16", glob, lambda l: synth.layer_weights(shape, l, "bf16"), max_window=max(rows),
+                     max_pos=P0 + NB * B + max(rows))
+    prompt = torch.from_numpy(synth.prompt_ids(shape, P0)).to(dev)
+
+    # latency table (window rows -> ms per step)
+    kv = dl.KVCache(model, P0 + max(rows))
+    dl.dllm_prefill(model.handle, kv.handle, prompt, P0)
+    tok0, mask0 = synth.window(shape, max(rows), range(max(rows)))
+    d_tok, d_mask = torch.from_numpy(tok0).to(dev), torch.from_numpy(mask0).to(dev)
+    ids = torch.empty(max(rows), dtype=torch.int32, device=dev)
+    conf = torch.empty(max(rows), device=dev)
+    table = []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for R in rows:
+        for _ in range(3):
+            dl.dllm_denoise_window(model.handle, kv.handle, P0, d_tok, d_mask, R, ids, conf)
+        e0.record()
+        for _ in range(10):
+            dl.dllm_denoise_window(model.handle, kv.handle, P0, d_tok, d_mask, R, ids, conf)
+        e1.record()
+        torch.cuda.synchronize()
+        table.append((R, e0.elapsed_time(e1) / 10))
+    kv.close()
+    log("latency table " + ", ".join(f"{r}: {t:.3f} ms" for r, t in table))
+
+    def generate(theta):
+        kv = dl.KVCache(model, P0 + NB * B)
+        dl.dllm_prefill(model.handle, kv.handle, prompt, P0)
+        gen = MBSDGenerator(model, kv, NB * B, window=WN, k=1, tau=4, latency_table=table, allowance=0.1,
+                            theta_accept=theta)
+        gen.run()
+        torch.cuda.synchronize()
+        kv.close()
+        tr = gen.trace
+        return dict(steps=len(tr), accepted=sum(len(e["accepted"]) for e in tr),
+                    lookahead_steps=sum(1 for e in tr if e["R"] > WN), rows_total=sum(e["W"] for e in tr))
+
+    runs = {}
+    for theta in (0.9, 0.0):
+        generate(theta)                          # warmup (untimed)
+        times = []
+        for _ in range(3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            st = generate(theta)
+            times.append(time.perf_counter() - t0)
+        runs[theta] = dict(st, latency_s=round(min(times), 4), latencies_s=[round(t, 4) for t in times])
+        log(f"mbsd theta {theta}: {runs[theta]}")
+    model.close()
+    main_run = runs[0.9]
+    lat = main_run["latency_s"]
+    return {
+        "metric": "end-to-end 128-token generation latency with multi-block speculative decoding, LLaDA-8B shape, "
+                  "block 32",
+        "value": round(128 / lat, 2), "unit": "tokens/s", "n_gpus": 1, "steps": main_run["steps"], "warmup": 1,
+        "ms_per_step": round(lat * 1000 / main_run["steps"], 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
+        "config": {"workload": E2E_MBSD, "prompt": P0, "blocks": NB, "block": B, "window": WN, "commits_per_step": 1,
+                   "tau": 4, "allowance": 0.1, "theta_accept": 0.9},
+        "latency_table_ms": [[r, round(t, 4)] for r, t in table],
+        "runs": {str(k): v for k, v in runs.items()},
+    }
+
+
 def run_sweep(args, dl, torch, shape, dev):
     """Step latency against the window's row count W (prefix 512, bf16): weight
     streaming keeps it nearly flat until the GEMMs become MFMA-bound."""
-    P, Ws = 512, [1, 2, 4, 8, 16, 32, 64, 128, 256]
+    P, Ws = 512, [1, 2, 4, 8, 16, 32, 40, 48, 64, 96, 128, 256]
     glob = synth.global_weights(shape, "bf16")
     model = dl.Model(shape, "bf16", glob, lambda l: synth.layer_weights(shape, l, "bf16"), max_window=max(Ws),
                      max_pos=P + max(Ws) + 64)
@@ -318,9 +398,11 @@ def measured_traffic(workload):
     return None
 
 
-def cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob):
-    """Oracle (float64 NumPy) on a bounded sample: one layer of the step plus the
-    full LM head, scaled to the whole 32-layer step."""
+def cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob, min_s=10.0):
+    """Oracle (float64 NumPy) on a bounded sample of the same step: whole steps whose
+    layer forward runs n_layers times on one layer's weights (every layer has the
+    same shapes, so the same arithmetic and memory traffic), then the final norm,
+    the LM head and the confidences; repeated until at least min_s seconds."""
     import oracle
 
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
@@ -331,16 +413,20 @@ def cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob):
     oracle.prefill(om, kv, prompt)        # setup, not timed
     P, W = wl["prefix"], wl["W"]
     ids = oracle.input_ids(shape, tok, mask)
-    t0 = time.perf_counter()
-    x, _ = oracle.forward_rows(om, kv, ids, P + np.arange(W), np.full(W, P + W), lm_head=False)
-    t1 = time.perf_counter()
-    logits = om.lm_logits(oracle.rmsnorm(x, om.final_norm, shape.eps))
-    oracle.confidence(logits)
-    t2 = time.perf_counter()
-    step_s = shape.n_layers * (t1 - t0) + (t2 - t1)
-    return {"value": 1.0 / step_s, "unit": "steps/s", "cores": cores, "kind": "oracle",
-            "sample": f"1 of {shape.n_layers} layers of the step ({t1 - t0:.2f} s) + the full LM head "
-                      f"({t2 - t1:.2f} s), layer time scaled x{shape.n_layers}; float64 NumPy"}
+    steps, t_layers, t_head = 0, 0.0, 0.0
+    while t_layers + t_head < min_s:
+        t0 = time.perf_counter()
+        for _ in range(shape.n_layers):
+            x, _ = oracle.forward_rows(om, kv, ids, P + np.arange(W), np.full(W, P + W), lm_head=False)
+        t1 = time.perf_counter()
+        logits = om.lm_logits(oracle.rmsnorm(x, om.final_norm, shape.eps))
+        oracle.confidence(logits)
+        t2 = time.perf_counter()
+        steps, t_layers, t_head = steps + 1, t_layers + (t1 - t0), t_head + (t2 - t1)
+    return {"value": steps / (t_layers + t_head), "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{steps} whole steps ({t_layers + t_head:.1f} s): the layer forward {shape.n_layers}x per "
+                      f"step on layer 0's weights ({t_layers / steps:.2f} s per step) + the full LM head and "
+                      f"confidences ({t_head / steps:.2f} s per step); float64 NumPy"}
 
 
 def main():
@@ -348,7 +434,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS) + [E2E, E2E_STAGED, E2E_MERGED])
+    ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS) + [E2E, E2E_STAGED, E2E_MERGED, E2E_MBSD])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 launches): the reference for HBM byte counters")
@@ -373,9 +459,10 @@ def main():
 
     import paper_2606_13740_amd as dl
 
-    if args.workload in (E2E, E2E_STAGED, E2E_MERGED):
+    if args.workload in (E2E, E2E_STAGED, E2E_MERGED, E2E_MBSD):
         torch.cuda.set_device(0)
-        run = {E2E: run_e2e, E2E_STAGED: run_e2e_staged, E2E_MERGED: run_e2e_merged}[args.workload]
+        run = {E2E: run_e2e, E2E_STAGED: run_e2e_staged, E2E_MERGED: run_e2e_merged,
+               E2E_MBSD: run_e2e_mbsd}[args.workload]
         print(json.dumps(run(args, dl, torch, synth.LLADA_8B, torch.device("cuda:0"))), flush=True)
         return
     if args.sweep:

@@ -87,7 +87,9 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
         const int k0 = kb * 32;
         char* base = lds + buf * BUF;
 #pragma unroll
-        for (int i = wave; i < NSLOT / 64; i += QG) {
+        for (int j = 0; j < (NSLOT / 64 + QG - 1) / QG; ++j) {
+            const int i = wave + j * QG;
+            if (i >= NSLOT / 64) break;
             const int sl = i * 64 + lane;
             const uint16_t* src;
             if (sl < KPLANE / 8) {                       // K: two planes of 32 x KCOLS slots

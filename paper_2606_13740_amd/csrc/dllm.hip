@@ -130,6 +130,7 @@ enum GemmKind { G_QKV = 0, G_RES = 1, G_GU = 2, G_LM = 3 };
 int pick_MT(int M) {
     if (M <= 16) return 1;
     if (M <= 32) return 2;
+    if (M <= 48) return 3;
     return 4;
 }
 
@@ -160,6 +161,7 @@ int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int K
     switch (MT) {
         case 1: launch_gemm_inst<WT, FW, NWn, NWk, 1>(g, epi, n_tiles, KS, gy, s); break;
         case 2: launch_gemm_inst<WT, FW, NWn, NWk, 2>(g, epi, n_tiles, KS, gy, s); break;
+        case 3: launch_gemm_inst<WT, FW, NWn, NWk, 3>(g, epi, n_tiles, KS, gy, s); break;
         case 4: launch_gemm_inst<WT, FW, NWn, NWk, 4>(g, epi, n_tiles, KS, gy, s); break;
         default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
     }
@@ -434,7 +436,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 dim3 grid(at.nsplit, H, nqg);
 #define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, QG_>), grid, dim3(QG_ * 64), 0, s, at)
 #define ATTN_QG(DH_) \
-    do { if (QG == 4) ATTN(DH_, 4); else if (QG == 2) ATTN(DH_, 2); else ATTN(DH_, 1); } while (0)
+    do { if (QG == 4) ATTN(DH_, 4); else if (QG == 3) ATTN(DH_, 3); else if (QG == 2) ATTN(DH_, 2); \
+         else ATTN(DH_, 1); } while (0)
                 if (Dh == 128) ATTN_QG(128); else ATTN_QG(64);
 #undef ATTN_QG
 #undef ATTN

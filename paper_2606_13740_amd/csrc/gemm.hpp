@@ -505,8 +505,12 @@ struct EpiLM {
                     logits[(size_t)m * V + n] = (n == mask_id) ? -INFINITY : Y[nl * ldy + ml];
             }
         }
-        const int tpt = blockDim.x / mcols;          // a power of two dividing 64
+        // lanes per token: the largest power of two <= blockDim.x / mcols (groups of
+        // tpt lanes are aligned inside a wave, so a group is wholly in or out of range)
+        int tpt = 1;
+        while (2 * tpt * mcols <= (int)blockDim.x && 2 * tpt <= 64) tpt *= 2;
         const int ml = threadIdx.x / tpt, sl = threadIdx.x % tpt;
+        if (ml >= mcols) return;
         const int per = (nrows + tpt - 1) / tpt;
         const int b = sl * per, e = min(nrows, b + per);
         LmPartial a{-INFINITY, -1, 0.f, 0.f};

@@ -101,7 +101,7 @@ def test_tiny_generation_with_resync(tiny):
     kv.close()
 
 
-@pytest.mark.parametrize("W", [1, 5, 16, 31, 33, 64, 100])
+@pytest.mark.parametrize("W", [1, 5, 16, 31, 33, 40, 48, 49, 64, 100])
 def test_micro_window_sizes(micro, W):
     model, om = micro
     sh = synth.MICRO
@@ -115,7 +115,7 @@ def test_micro_window_sizes(micro, W):
     kv.close()
 
 
-@pytest.mark.parametrize("W", [32, 64])
+@pytest.mark.parametrize("W", [32, 44, 48, 64])
 def test_small_lowp_step(small, W):
     model, om, dtype = small
     sh = SMALL
