@@ -348,6 +348,31 @@ def denoise_window(model: OracleModel, kv: OracleKV, w0: int, tok: np.ndarray, m
     return StepOut(logits, ids_out, conf, x)
 
 
+def skip_logits(out: StepOut, need: Optional[np.ndarray], n_need: int):
+    """Selective logits skipping (System Design, "Dual-Path Progressive Revision",
+    "Selective Logits Skipping"): the output projection, the confidence and the
+    selection run only for positions whose identity or confidence can still matter;
+    the other positions are skipped.  `need` flags those rows (None: every row);
+    at most n_need of them are evaluated, the first ones in row order.  A skipped
+    row reports id -1 and confidence 0.  Returns (ids, conf)."""
+    W = len(out.ids)
+    flag = np.ones(W, dtype=bool) if need is None else (np.asarray(need) != 0)
+    chosen = np.zeros(W, dtype=bool)
+    chosen[np.flatnonzero(flag)[:max(0, n_need)]] = True
+    ids = np.where(chosen, out.ids, -1).astype(np.int64)
+    conf = np.where(chosen, out.conf, 0.0)
+    return ids, conf
+
+
+def denoise_window_sls(model: OracleModel, kv: OracleKV, w0: int, tok: np.ndarray, mask: np.ndarray,
+                       need: Optional[np.ndarray], n_need: int):
+    """denoise_window with selective logits skipping: the forward (and the K/V it
+    writes) is the window step's; only the rows skip_logits keeps get an output."""
+    out = denoise_window(model, kv, w0, tok, mask)
+    ids, conf = skip_logits(out, need, n_need)
+    return ids, conf, out
+
+
 def commit(conf: np.ndarray, pred: np.ndarray, tok: np.ndarray, mask: np.ndarray,
            seg_begin: int, seg_len: int, k: int):
     """Commit the k most confident masked positions of [seg_begin, seg_begin + seg_len).

@@ -270,6 +270,58 @@ def test_window_permutation_permutes_outputs():
 
 
 # ----------------------------------------------------------------------------
+# Selective logits skipping
+# ----------------------------------------------------------------------------
+
+
+def test_skip_logits_brute_force_over_every_need_mask():
+    W = 5
+    rng = np.random.default_rng(3)
+    out = om.StepOut(logits=None, ids=rng.integers(0, 50, W), conf=rng.random(W), x=None)
+    for bits in itertools.product([0, 1], repeat=W):
+        need = np.array(bits, np.uint8)
+        for n_need in range(W + 2):
+            ids, conf = oracle.skip_logits(out, need, n_need)
+            seen = 0
+            for i in range(W):
+                keep = bits[i] == 1 and seen < n_need
+                seen += bits[i]
+                assert ids[i] == (out.ids[i] if keep else -1)
+                assert conf[i] == (out.conf[i] if keep else 0.0)
+    ids, conf = oracle.skip_logits(out, None, W)
+    np.testing.assert_array_equal(ids, out.ids)
+    np.testing.assert_array_equal(conf, out.conf)
+    ids, conf = oracle.skip_logits(out, None, 2)
+    assert list(ids[2:]) == [-1] * (W - 2) and list(ids[:2]) == list(out.ids[:2])
+
+
+def test_sls_window_is_full_forward_on_kept_rows_and_leaves_the_cache_as_the_step():
+    sh = MICRO
+    model, _ = micro_model(sh)
+    P0 = 20
+    kv, seq = _build_prefix(model, sh, P0, 1, P0 + 2 * sh.block)
+    W = sh.block
+    tok, mask = synth.window(sh, W, list(range(8, 32)))
+    need = mask.copy()
+    need[[9, 30]] = 0
+    kv_full = kv.copy()
+    P = kv.prefix_len
+    ids, conf, _ = oracle.denoise_window_sls(model, kv, P, tok, mask, need, 15)
+    oracle.denoise_window(model, kv_full, P, tok, mask)
+    np.testing.assert_array_equal(kv.K, kv_full.K)
+    np.testing.assert_array_equal(kv.V, kv_full.V)
+    full_seq = np.concatenate([seq, oracle.input_ids(sh, tok, mask)])
+    allowed = oracle.block_causal_allowed(len(full_seq), P0, sh.block, window_from=len(seq))
+    _, logits, _, _ = oracle.forward_full(model, full_seq, allowed)
+    ref_ids, ref_conf = oracle.confidence(logits[len(seq):])
+    kept = np.flatnonzero(need)[:15]
+    skipped = np.setdiff1d(np.arange(W), kept)
+    np.testing.assert_array_equal(ids[kept], ref_ids[kept])
+    np.testing.assert_allclose(conf[kept], ref_conf[kept], rtol=1e-10)
+    assert np.all(ids[skipped] == -1) and np.all(conf[skipped] == 0.0)
+
+
+# ----------------------------------------------------------------------------
 # Refresh special cases
 # ----------------------------------------------------------------------------
 
