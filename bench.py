@@ -31,9 +31,9 @@ WORKLOADS = {
     "llada8b_bf16_p512_w32": dict(shape="llada8b", dtype="bf16", prefix=512, W=32,
                                   masked=list(range(8, 32)), segs=[(0, 32, 1)]),
     "llada8b_bf16_p1024_w64_spec": dict(shape="llada8b", dtype="bf16", prefix=1024, W=64,
-                                        masked=list(range(24, 64)), segs=[(0, 32, 4), (32, 32, 4)]),
+                                        masked=list(range(24, 64)), segs=[(0, 32, 4), (32, 32, 4)], sls=True),
     "llada8b_w8_p4096_w64_spec": dict(shape="llada8b", dtype="w8", prefix=4096, W=64,
-                                      masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)]),
+                                      masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)], sls=True),
 }
 DEFAULT = "llada8b_bf16_p512_w32"
 E2E = "llada8b_bf16_e2e128"      # end-to-end 128-token generation (prefill included)
@@ -243,8 +243,9 @@ def run_e2e_mbsd(args, dl, torch, shape, dev):
     speculative decoding: a 32-row window slides along the commit frontier, one
     commit per step, the window grows by the latency table once at most 4 masked
     positions remain in the current block (allowance 10%), draft rows past the
-    current block are recorded and accepted when their block becomes current.  The
-    latency table is measured first: dllm_denoise_window at each row count.  Run
+    current block are recorded and accepted when their block becomes current; only
+    masked window rows get an LM-head output (selective logits skipping).  The
+    latency table is measured first: the window at each row count.  Run
     twice: acceptance threshold 0.9 (random weights give confidences near 1e-3, so
     nothing is accepted: the mechanism's cost) and 0 (a draft is accepted whenever
     the current step predicts the id it recorded)."""
@@ -264,14 +265,18 @@ def run_e2e_mbsd(args, dl, torch, shape, dev):
     d_tok, d_mask = torch.from_numpy(tok0).to(dev), torch.from_numpy(mask0).to(dev)
     ids = torch.empty(max(rows), dtype=torch.int32, device=dev)
     conf = torch.empty(max(rows), device=dev)
+    # at a lookahead step at most tau = 4 current-block rows and the R - 32 draft rows
+    # are masked: the table times the window with that many LM-head rows
+    need = torch.zeros(max(rows), dtype=torch.uint8, device=dev)
+    need[WN - 4:] = 1
     table = []
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     for R in rows:
         for _ in range(3):
-            dl.dllm_denoise_window(model.handle, kv.handle, P0, d_tok, d_mask, R, ids, conf)
+            dl.dllm_denoise_window_sls(model.handle, kv.handle, P0, d_tok, d_mask, need, R - WN + 4, R, ids, conf)
         e0.record()
         for _ in range(10):
-            dl.dllm_denoise_window(model.handle, kv.handle, P0, d_tok, d_mask, R, ids, conf)
+            dl.dllm_denoise_window_sls(model.handle, kv.handle, P0, d_tok, d_mask, need, R - WN + 4, R, ids, conf)
         e1.record()
         torch.cuda.synchronize()
         table.append((R, e0.elapsed_time(e1) / 10))
@@ -436,6 +441,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS) + [E2E, E2E_STAGED, E2E_MERGED, E2E_MBSD])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sls", action="store_true",
+                    help="run the LM head over every window row (no selective logits skipping)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 launches): the reference for HBM byte counters")
     ap.add_argument("--sweep", action="store_true",
@@ -495,8 +502,16 @@ def main():
     torch.cuda.synchronize()
     log(f"prefill {P} done")
 
+    # selective logits skipping: only masked rows need an LM-head output; the bound is
+    # the masked count at the start (commits only shrink the set)
+    sls = wl.get("sls", False) and not args.no_sls
+    n_need = len(wl["masked"])
+
     def step():
-        dl.dllm_denoise_step(model.handle, kv.handle, d_tok, d_mask, W, ids, conf)
+        if sls:
+            dl.dllm_denoise_window_sls(model.handle, kv.handle, P, d_tok, d_mask, d_mask, n_need, W, ids, conf)
+        else:
+            dl.dllm_denoise_step(model.handle, kv.handle, d_tok, d_mask, W, ids, conf)
         for j, (b, n, k) in enumerate(wl["segs"]):
             dl.dllm_commit(conf, ids, d_tok, d_mask, b, n, k, cpos[16 * j:], ncom[j:])
 
@@ -558,7 +573,8 @@ def main():
         "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
         "config": {"workload": args.workload, "layers": shape.n_layers, "d_model": shape.d_model,
                    "heads": shape.n_heads, "head_dim": shape.head_dim, "d_ff": shape.d_ff, "vocab": shape.vocab,
-                   "prefix": P, "window": W, "masked": len(wl["masked"]), "commits_per_step": commits},
+                   "prefix": P, "window": W, "masked": len(wl["masked"]), "commits_per_step": commits,
+                   "lm_head_rows": n_need if sls else W},
         "query_tok_s": round(W * steps_s, 1),
         "committed_tok_s": round(commits * steps_s, 1),
         "step_hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -216,7 +216,9 @@ int dllm_refresh_kv(dllm_model* m, dllm_kv* kv, const int32_t* d_pos, const int3
  *   - the last W rows: the window d_tok / d_mask (nullable) at positions
  *     P + n_block.., keys [0, P + n_block + W), as dllm_denoise_step.
  * A refresh position inside the block being appended is expressed by appending
- * the block with the revised id.  Outputs (each pair both set or both NULL):
+ * the block with the revised id.  The LM head runs only over the rows whose
+ * outputs are asked for (never the appended block's).  Outputs (each pair both set
+ * or both NULL):
  * d_out_id / d_out_conf [W] for the window, d_ref_out_id / d_ref_out_conf [n_ref]
  * for the refresh rows.  prefix_len becomes P + n_block.  Any group may be empty;
  * E_INVAL unless 1 <= n_ref + n_block + W <= max_window and the refresh positions
@@ -239,6 +241,22 @@ int dllm_step_merged(dllm_model* m, dllm_kv* kv, const int32_t* d_ref_pos, const
 int dllm_denoise_window(dllm_model* m, dllm_kv* kv, int32_t w0, const int32_t* d_tok,
                         const uint8_t* d_mask, int32_t W, int32_t* d_out_id, float* d_out_conf,
                         dllm_stream stream);
+
+/* dllm_denoise_window with selective logits skipping (System Design, "Dual-Path
+ * Progressive Revision", "Selective Logits Skipping": the output projection, the
+ * confidence and the selection are computed only for positions whose identity or
+ * confidence can still change a decision; stable positions skip them).  The
+ * forward and the K/V it writes are dllm_denoise_window's.  d_need (device, W
+ * bytes; NULL = every row) flags the rows that need an output, e.g. the mask of a
+ * top-k step (committed rows are final) or the non-stable rows of a staged step.
+ * The LM head then runs over at most n_need rows, the first flagged ones in row
+ * order, packed together, so its cost follows n_need rather than W; each of those
+ * rows gets the (id, conf) dllm_denoise_window would give it, every other row gets
+ * id -1 and conf 0.  n_need = 0 skips the LM head.  E_INVAL unless
+ * 0 <= n_need <= W, plus dllm_denoise_window's checks. */
+int dllm_denoise_window_sls(dllm_model* m, dllm_kv* kv, int32_t w0, const int32_t* d_tok,
+                            const uint8_t* d_mask, const uint8_t* d_need, int32_t n_need, int32_t W,
+                            int32_t* d_out_id, float* d_out_conf, dllm_stream stream);
 
 /* Parity only (never on the timed path): the same step as dllm_denoise_step, also
  * writing the full logits d_logits[W][vocab] (float, MASK column = -inf).  If

@@ -64,6 +64,7 @@ _SIGNATURES = {
     "dllm_append_prefix_kv": ([_vp, _vp, _vp, _i32, _vp], ctypes.c_int),
     "dllm_refresh_kv": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_denoise_window": ([_vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_denoise_window_sls": ([_vp, _vp, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_accept_drafts": ([_vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _vp, _vp, _vp], ctypes.c_int),
     "dllm_record_drafts": ([_vp, _vp, _vp, _i32, _vp], ctypes.c_int),
     "dllm_step_merged": ([_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp],
@@ -183,6 +184,12 @@ def dllm_refresh_kv(model: int, kv: int, pos, new_ids, n: int, out_id=None, out_
 def dllm_denoise_window(model: int, kv: int, w0: int, tok, mask, W: int, out_id, out_conf, stream=None):
     _check(lib().dllm_denoise_window(model, kv, w0, _ptr(tok), _ptr(mask), W, _ptr(out_id), _ptr(out_conf),
                                      _stream(stream)), "dllm_denoise_window")
+
+
+def dllm_denoise_window_sls(model: int, kv: int, w0: int, tok, mask, need, n_need: int, W: int, out_id, out_conf,
+                            stream=None):
+    _check(lib().dllm_denoise_window_sls(model, kv, w0, _ptr(tok), _ptr(mask), _ptr(need), n_need, W, _ptr(out_id),
+                                         _ptr(out_conf), _stream(stream)), "dllm_denoise_window_sls")
 
 
 def dllm_accept_drafts(conf, ids, draft_ids, tok, mask, n: int, theta: float, accepted_pos=None, n_accepted=None,

@@ -79,6 +79,7 @@ struct Workspace {
     uint8_t* msk = nullptr;  // [rows] mask flags of a merged pass
     int* oid = nullptr;      // [rows] argmax ids of a merged pass
     float* oconf = nullptr;  // [rows] confidences of a merged pass
+    uint8_t* need = nullptr; // [rows] LM-head row flags of a merged pass
 };
 
 constexpr int MAX_SPLIT = 16;
@@ -221,7 +222,7 @@ struct ProbeScope {
 // ---------------------------------------------------------------------------
 
 void free_ws(Workspace& w) {
-    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart, w.tok, w.msk, w.oid, w.oconf};
+    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart, w.tok, w.msk, w.oid, w.oconf, w.need};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     w = Workspace{};
@@ -268,6 +269,7 @@ int ensure_ws(dllm_model* m, int rows_needed) {
     ALLOC(w.msk, (size_t)rows);
     ALLOC(w.oid, (size_t)rows * 4);
     ALLOC(w.oconf, (size_t)rows * 4);
+    ALLOC(w.need, (size_t)rows);
 #undef ALLOC
     return DLLM_OK;
 }
@@ -347,13 +349,16 @@ struct FwdArgs {
     int* out_id;
     float* out_conf;
     float* xout;              // residual copy or nullptr
+    bool sel;                 // LM head over selected rows only (selective logits skipping)
+    const uint8_t* need;      // device row flags (nullable: every row) when sel
+    int n_sel;                // at most this many flagged rows get an LM output
 };
 
 // O / down projection: split-K GEMM into partials, then the reduction that adds
 // them to the residual and prepares the next RMSNorm's operand and partial sums.
 template <int WT, bool XF32>
 int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* gnext, int M, int Mc, int MT, int gy,
-                  hipStream_t s) {
+                  hipStream_t s, bool sel = false, const uint8_t* need = nullptr, int n_sel = 0) {
     Workspace& w = m->ws;
     const int d = m->cfg.d_model;
     const int KS = (Mc <= 64 && big(G_RES, W.n_tiles)) ? RES_SPLIT : 1;
@@ -363,7 +368,7 @@ int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* g
     int rc = launch_gemm<WT, G_RES>(W.n_tiles, MT, KS, g, e, gy, s);
     if (rc) return rc;
     hipLaunchKernelGGL((residual_reduce_kernel<XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const float*)w.part, KS, Mc, d,
-                       M, m->cfg.eps, w.x, gnext, w.xg, m->KCx_d);
+                       M, m->cfg.eps, w.x, gnext, w.xg, m->KCx_d, sel, need, n_sel);
     return DLLM_OK;
 }
 
@@ -461,23 +466,33 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         }
         // down projection + residual (+ next norm operand)
         {
-            const float* gnext = (l + 1 < c.n_layers) ? m->layers[l + 1].g1 : m->gf;
+            const bool last = (l + 1 == c.n_layers);
+            const float* gnext = last ? m->gf : m->layers[l + 1].g1;
+            const bool sel = last && a.lm && a.sel;
             ProbeScope ps(m, DLLM_K_DOWN, s);
-            if ((rc = residual_proj<WT, XF32>(m, L.down, w.af, gnext, a.M, Mc, MT, gy, s))) return rc;
+            if ((rc = residual_proj<WT, XF32>(m, L.down, w.af, gnext, a.M, Mc, MT, gy, s, sel, a.need, a.n_sel)))
+                return rc;
         }
     }
     if (a.xout) HIP_TRY(hipMemcpyAsync(a.xout, w.x, (size_t)a.M * d * 4, hipMemcpyDeviceToDevice, s));
     if (a.lm) {
-        if (Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
+        // rows the LM head runs over: all M, or the selected ones packed to the front
+        const int Ml = a.sel ? std::min(a.n_sel, a.M) : a.M;
+        int MTl = MT, gyl = gy;
+        if (a.sel) {
+            if (Ml <= 64) { MTl = pick_MT(std::max(Ml, 1)); gyl = 1; }
+            else { MTl = 4; gyl = ceil_div(Ml, 64); }
+        }
+        if (gyl * MTl * 16 > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
         GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles};
         const int gx = row_groups(G_LM, m->lm.n_tiles);
-        EpiLM e{c.vocab, c.mask_id, a.M, w.lm, w.wrows, a.logits};
-        {
+        if (Ml > 0) {
+            EpiLM e{c.vocab, c.mask_id, Ml, w.lm, w.wrows, a.logits};
             ProbeScope ps(m, DLLM_K_LMHEAD, s);
-            if ((rc = launch_gemm<WT, G_LM>(m->lm.n_tiles, MT, 1, g, e, gy, s))) return rc;
+            if ((rc = launch_gemm<WT, G_LM>(m->lm.n_tiles, MTl, 1, g, e, gyl, s))) return rc;
         }
         hipLaunchKernelGGL(lm_combine_kernel, dim3(a.M), dim3(64), 0, s, (const LmPartial*)w.lm, gx, w.wrows,
-                           a.out_id, a.out_conf);
+                           a.out_id, a.out_conf, a.sel, a.need, a.n_sel, a.M);
     }
     HIP_TRY(hipGetLastError());
     return DLLM_OK;
@@ -715,6 +730,23 @@ int dllm_denoise_window(dllm_model* m, dllm_kv* kv, int32_t w0, const int32_t* d
     return forward(m, kv, a, (hipStream_t)stream);
 }
 
+int dllm_denoise_window_sls(dllm_model* m, dllm_kv* kv, int32_t w0, const int32_t* d_tok, const uint8_t* d_mask,
+                            const uint8_t* d_need, int32_t n_need, int32_t W, int32_t* d_out_id, float* d_out_conf,
+                            dllm_stream stream) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (!d_tok || !d_out_id || !d_out_conf) return fail(DLLM_E_INVAL, "NULL argument");
+    if (W < 1 || W > m->cfg.max_window) return fail(DLLM_E_INVAL, "W must be in [1, max_window]");
+    if (n_need < 0 || n_need > W) return fail(DLLM_E_INVAL, "n_need must be in [0, W]");
+    if (w0 < kv->prefix_len) return fail(DLLM_E_INVAL, "w0 must be >= prefix_len");
+    if ((long)w0 + W > kv->capacity) return fail(DLLM_E_CAPACITY, "w0 + W exceeds the cache capacity");
+    FwdArgs a{};
+    a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = w0; a.T = w0 + W;
+    a.n_layers = m->cfg.n_layers; a.lm = true; a.out_id = d_out_id; a.out_conf = d_out_conf;
+    a.sel = true; a.need = d_need; a.n_sel = n_need;
+    return forward(m, kv, a, (hipStream_t)stream);
+}
+
 int dllm_debug_logits(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
                       float* d_logits, int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
     int rc = window_checks(m, kv, d_tok, W);
@@ -823,13 +855,18 @@ int dllm_step_merged(dllm_model* m, dllm_kv* kv, const int32_t* d_ref_pos, const
     }
     if ((rc = ensure_ws(m, M))) return rc;
     Workspace& w = m->ws;
+    // the LM head runs only over the rows whose outputs are asked for (the appended
+    // block's rows never need one)
+    const bool ref_out = d_ref_out_id != nullptr && n_ref > 0, win_out = d_out_id != nullptr && W > 0;
     hipLaunchKernelGGL(merged_rows_kernel, dim3(ceil_div(M, 64)), dim3(64), 0, s, d_ref_pos, d_ref_id, n_ref,
-                       d_block_tok, n_block, d_tok, d_mask, W, P, kv->prompt_len, m->cfg.block, w.tok, w.msk, w.pos,
-                       w.lim);
-    const bool lm = (d_out_id != nullptr && W > 0) || (d_ref_out_id != nullptr && n_ref > 0);
+                       d_block_tok, n_block, d_tok, d_mask, W, P, kv->prompt_len, m->cfg.block, (int)ref_out,
+                       (int)win_out, w.tok, w.msk, w.pos, w.lim, w.need);
+    const bool lm = ref_out || win_out;
+    const int n_sel = (ref_out ? n_ref : 0) + (win_out ? W : 0);
     FwdArgs a{};
     a.M = M; a.tok = w.tok; a.mask = w.msk; a.pos = w.pos; a.T = P + n_block + W; a.lim = w.lim;
     a.n_layers = m->cfg.n_layers; a.lm = lm; a.out_id = w.oid; a.out_conf = w.oconf;
+    a.sel = n_sel < M; a.need = w.need; a.n_sel = n_sel;
     if ((rc = forward(m, kv, a, s))) return rc;
     if (lm) {
         hipLaunchKernelGGL(merged_out_kernel, dim3(ceil_div(M, 64)), dim3(64), 0, s, (const int*)w.oid,

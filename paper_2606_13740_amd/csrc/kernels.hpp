@@ -77,15 +77,34 @@ embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int
     write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red);
 }
 
+// Row selection of the LM head (selective logits skipping): row m of M is kept if
+// it is flagged (need[m] != 0; every row when need is NULL) and fewer than n_sel
+// flagged rows precede it; a kept row's slot is that count.  Returns -1 for a row
+// that is not kept.  Every thread of the block gets the same answer.
+template <int NT>
+__device__ __forceinline__ int lm_slot(const uint8_t* need, int n_sel, int M, int m, float* red) {
+    if (need == nullptr) return (m < M && m < n_sel) ? m : -1;
+    float c = 0.f;
+    for (int i = threadIdx.x; i < m && i < M; i += NT) c += need[i] ? 1.f : 0.f;
+    const int before = (int)block_sum<NT>(c, red);
+    return (m < M && need[m] && before < n_sel) ? before : -1;
+}
+
 // Split-K reduction of a residual projection (O or down), one workgroup per row:
 //   x[m][n] += sum_ks P[ks][m][n]   (fixed order),
-// then the next RMSNorm's normalised operand.  Padding rows get zeros.
+// then the next RMSNorm's normalised operand.  Padding rows get zeros.  With
+// `sel` set (the last layer feeding a selective LM head) the operand of a kept row
+// goes to its slot (lm_slot) and other rows write none.
 template <bool XF32>
 __global__ void __launch_bounds__(ROW_NT)
 residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps, float* x, const float* g,
-                       void* xg, int KCx) {
+                       void* xg, int KCx, bool sel, const uint8_t* need, int n_sel) {
     __shared__ float red[ROW_NT / 64];
     const int m = blockIdx.x;
+    int dst = m;
+    if (sel) {
+        dst = lm_slot<ROW_NT>(need, n_sel, M, m, red);
+    }
     float4 xv[ROW_VPT];
 #pragma unroll
     for (int j = 0; j < ROW_VPT; ++j) {
@@ -107,7 +126,7 @@ residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps
         }
         xv[j] = v;
     }
-    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red);
+    if (dst >= 0) write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, dst, d, eps, g, xg, KCx, red);
 }
 
 // Streaming read of n 16-byte units (measurement helper): grid-stride, 4 loads in flight per lane.
@@ -144,10 +163,25 @@ __device__ __forceinline__ LmPartial lm_merge(LmPartial a, LmPartial b) {
     return o;
 }
 
+// One workgroup per window row m.  With `sel`, row m reads the partials of its LM
+// slot (lm_slot); a row without one reports id -1 and confidence 0.
 __global__ void __launch_bounds__(64)
-lm_combine_kernel(const LmPartial* part, int n_wg, int part_ld, int* out_id, float* out_conf) {
-    const int m = blockIdx.x;
+lm_combine_kernel(const LmPartial* part, int n_wg, int part_ld, int* out_id, float* out_conf, bool sel,
+                  const uint8_t* need, int n_sel, int M) {
+    __shared__ float red[1];
     const int lane = threadIdx.x;
+    int m = blockIdx.x;
+    if (sel) {
+        const int slot = lm_slot<64>(need, n_sel, M, blockIdx.x, red);
+        if (slot < 0) {
+            if (lane == 0) {
+                if (out_id) out_id[blockIdx.x] = -1;
+                if (out_conf) out_conf[blockIdx.x] = 0.f;
+            }
+            return;
+        }
+        m = slot;
+    }
     LmPartial acc{-INFINITY, -1, 0.f, 0.f};
     for (int w0 = lane; w0 < n_wg; w0 += 64 * 8) {
         LmPartial q[8];
@@ -170,8 +204,8 @@ lm_combine_kernel(const LmPartial* part, int n_wg, int part_ld, int* out_id, flo
         acc = (lane & off) ? lm_merge(o, acc) : lm_merge(acc, o);
     }
     if (lane == 0) {
-        if (out_id) out_id[m] = acc.arg;
-        if (out_conf) out_conf[m] = 1.0f / acc.s;
+        if (out_id) out_id[blockIdx.x] = acc.arg;
+        if (out_conf) out_conf[blockIdx.x] = 1.0f / acc.s;
     }
 }
 
@@ -433,9 +467,12 @@ __global__ void record_drafts_kernel(const int* id, const uint8_t* mask, int* dr
 // are revised prefix positions (keys up to the end of their block, capped at P),
 // rows [n_ref, n_ref + n_blk) the completed block at P.. (keys [0, P + n_blk)),
 // the last W rows the window at P + n_blk.. (keys [0, P + n_blk + W), mask kept).
+// need: the rows whose (id, conf) is asked for (refresh rows if ref_out, window
+// rows if win_out; the appended block never).
 __global__ void merged_rows_kernel(const int* ref_pos, const int* ref_id, int n_ref, const int* blk, int n_blk,
                                    const int* tok, const uint8_t* mask, int W, int P, int prompt_len, int block,
-                                   int* otok, uint8_t* omask, int* opos, int* olim) {
+                                   int ref_out, int win_out, int* otok, uint8_t* omask, int* opos, int* olim,
+                                   uint8_t* oneed) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n_ref + n_blk + W) return;
     int t, p, l;
@@ -461,6 +498,7 @@ __global__ void merged_rows_kernel(const int* ref_pos, const int* ref_id, int n_
     omask[i] = mk;
     opos[i] = p;
     olim[i] = l;
+    oneed[i] = (uint8_t)(i < n_ref ? ref_out : (i < n_ref + n_blk ? 0 : win_out));
 }
 
 // Outputs of a merged pass: the refresh rows' and the window rows' (id, conf).

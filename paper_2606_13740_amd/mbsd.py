@@ -22,18 +22,22 @@ Policy (the readings of the passage this module takes):
     that the window holds;
   * adaptive lookahead: once at most `tau` masked positions remain in the current
     block, the window takes the largest row count of the latency table whose
-    latency stays within (1 + allowance) of the base window's.
+    latency stays within (1 + allowance) of the base window's;
+  * with `sls` (selective logits skipping), only the window's masked rows get an
+    LM-head output: a committed row's prediction is never used again (commits,
+    acceptance and draft records read masked rows only).
 """
 import numpy as np
 import torch
 
-from . import dllm_accept_drafts, dllm_commit, dllm_denoise_window, dllm_kv_set_prefix_len, dllm_record_drafts
+from . import (dllm_accept_drafts, dllm_commit, dllm_denoise_window, dllm_denoise_window_sls, dllm_kv_set_prefix_len,
+               dllm_record_drafts)
 
 
 class MBSDGenerator:
     def __init__(self, model, kv, n_gen: int, window: int = 32, k: int = 1, tau: int = 4, latency_table=None,
                  allowance: float = 0.1, theta_accept: float = 0.9, stream=None, device: str = "cuda",
-                 record: bool = False):
+                 record: bool = False, sls: bool = True):
         sh = model.shape
         self.model, self.kv = model, kv
         self.B, self.mask_id = sh.block, sh.mask_id
@@ -46,7 +50,7 @@ class MBSDGenerator:
         self.Wn, self.k, self.tau = window, k, tau
         self.table = sorted(latency_table) if latency_table else [(window, 1.0)]
         self.allowance, self.theta = allowance, float(theta_accept)
-        self.stream, self.dev, self.record = stream, device, record
+        self.stream, self.dev, self.record, self.sls = stream, device, record, sls
         self.tok = torch.full((n_gen,), self.mask_id, dtype=torch.int32, device=device)
         self.mask = torch.ones(n_gen, dtype=torch.uint8, device=device)
         self.draft = torch.full((n_gen,), -1, dtype=torch.int32, device=device)
@@ -84,7 +88,12 @@ class MBSDGenerator:
             if self.record:
                 rec = dict(step=t, w0=w0, W=W, R=R, remaining=remaining, tok=self.tok[a:a + W].cpu().numpy(),
                            mask=self.mask[a:a + W].cpu().numpy())
-            dllm_denoise_window(h, kvh, w0, self.tok[a:], self.mask[a:], W, ids, conf, self.stream)
+            if self.sls:
+                n_need = int(masked[a:a + W].sum())
+                dllm_denoise_window_sls(h, kvh, w0, self.tok[a:], self.mask[a:], self.mask[a:], n_need, W, ids, conf,
+                                        self.stream)
+            else:
+                dllm_denoise_window(h, kvh, w0, self.tok[a:], self.mask[a:], W, ids, conf, self.stream)
             cur = min(P + B, w0 + W) - w0
             acc = np.zeros(0, dtype=np.int64)
             if fresh:

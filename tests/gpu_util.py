@@ -77,6 +77,8 @@ def assert_ids_match_where_decided(got_ids, ref_logits, err_bound, ref_conf=None
     """Argmax must match wherever the oracle's top-2 logit gap exceeds 2 * err_bound
     (two logits each off by at most err_bound cannot swap), and wherever its top-2
     probability margin exceeds 1e-3.  Returns the fraction of rows decided."""
+    if len(got_ids) == 0:
+        return 1.0
     srt = np.sort(ref_logits, axis=-1)
     gap = srt[:, -1] - srt[:, -2]
     ref_ids = np.argmax(ref_logits, axis=-1)

@@ -92,7 +92,8 @@ def test_accept_and_record_drafts_bit_exact(n):
         np.testing.assert_array_equal(rec.cpu().numpy(), r2)
 
 
-def test_driver_run_replays_in_the_oracle():
+@pytest.mark.parametrize("sls", [False, True])
+def test_driver_run_replays_in_the_oracle(sls):
     from paper_2606_13740_amd.mbsd import MBSDGenerator
 
     sh = synth.TINY
@@ -102,9 +103,9 @@ def test_driver_run_replays_in_the_oracle():
     kv = dl.KVCache(model, P0 + n_gen)
     prompt = synth.prompt_ids(sh, P0)
     dl.dllm_prefill(model.handle, kv.handle, dev_i32(prompt), P0)
-    print("case: MBSD driver, tiny fp32, 2 blocks", flush=True)
+    print(f"case: MBSD driver, tiny fp32, 2 blocks, sls {sls}", flush=True)
     gen = MBSDGenerator(model, kv, n_gen, window=32, k=k, tau=tau, latency_table=table, allowance=0.1,
-                        theta_accept=0.0, record=True)
+                        theta_accept=0.0, record=True, sls=sls)
     final = gen.run()
     tr = gen.trace
     assert np.all(final != sh.mask_id) and kv.prefix_len == P0 + n_gen
@@ -118,8 +119,12 @@ def test_driver_run_replays_in_the_oracle():
         a = w0 - P0
         assert w0 >= P and e["W"] == min(e["R"], P0 + n_gen - w0)
         so = oracle.denoise_window(om, okv, w0, e["tok"], e["mask"])
-        np.testing.assert_allclose(e["conf"], so.conf, rtol=1e-3)
-        assert_ids_match_where_decided(e["ids"], so.logits, 1e-4)
+        rows = np.flatnonzero(e["mask"]) if sls else np.arange(W)      # rows with an output
+        np.testing.assert_allclose(e["conf"][rows], so.conf[rows], rtol=1e-3)
+        assert_ids_match_where_decided(e["ids"][rows], so.logits[rows], 1e-4)
+        if sls:
+            off = np.flatnonzero(e["mask"] == 0)
+            assert np.all(e["ids"][off] == -1) and np.all(e["conf"][off] == 0.0)
         # the GPU's confidences under the oracle's policy functions give the same decisions
         cur = min(P + B, w0 + W) - w0
         tok, mask = e["tok"].astype(np.int64).copy(), e["mask"].copy()
