@@ -81,15 +81,24 @@ def softmax(s: np.ndarray) -> np.ndarray:
     return e / np.sum(e, axis=-1, keepdims=True)
 
 
+def group_heads(KV: np.ndarray, n_heads: int) -> np.ndarray:
+    """Grouped-query attention: K or V [keys, Hkv, Dh] seen by n_heads query heads;
+    query head h reads K/V head h // (n_heads / Hkv).  Hkv = n_heads is plain
+    multi-head attention."""
+    G = n_heads // KV.shape[1]
+    return np.repeat(KV, G, axis=1)
+
+
 def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray, limits: np.ndarray) -> np.ndarray:
-    """Row i (all heads) attends to keys [0, limits[i]) of K, V [keys, H, Dh]."""
+    """Row i (all heads) attends to keys [0, limits[i]) of K, V [keys, Hkv, Dh]
+    (query head h uses K/V head h // (H / Hkv))."""
     n, H, dh = q.shape
     out = np.zeros_like(q)
     scale = 1.0 / np.sqrt(dh)
     for i in range(n):
         lim = int(limits[i])
-        k = K[:lim]                                         # [lim, H, Dh]
-        v = V[:lim]
+        k = group_heads(K[:lim], H)                         # [lim, H, Dh]
+        v = group_heads(V[:lim], H)
         s = np.einsum("hd,khd->hk", q[i], k) * scale        # [H, lim]
         p = softmax(s)
         out[i] = np.einsum("hk,khd->hd", p, v)
@@ -101,11 +110,12 @@ def attend_masked(q: np.ndarray, K: np.ndarray, V: np.ndarray, allowed: np.ndarr
     n, H, dh = q.shape
     out = np.zeros_like(q)
     scale = 1.0 / np.sqrt(dh)
+    Kg, Vg = group_heads(K, H), group_heads(V, H)
     for i in range(n):
         idx = np.nonzero(allowed[i])[0]
-        s = np.einsum("hd,khd->hk", q[i], K[idx]) * scale
+        s = np.einsum("hd,khd->hk", q[i], Kg[idx]) * scale
         p = softmax(s)
-        out[i] = np.einsum("hk,khd->hd", p, V[idx])
+        out[i] = np.einsum("hk,khd->hd", p, Vg[idx])
     return out
 
 
@@ -152,6 +162,7 @@ def dequantize_rows(q: np.ndarray, s: np.ndarray) -> np.ndarray:
 
 
 GEMM_WEIGHTS = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+QKV_BIASES = ("bq", "bk", "bv")
 
 
 def _f64(a: np.ndarray) -> np.ndarray:
@@ -198,6 +209,8 @@ class OracleModel:
             return self._cache[l]
         src = self._layer_source(l) if self._layer_source is not None else self._src["layers"][l]
         out = {k: self._convert_matrix(src[k]) for k in GEMM_WEIGHTS}
+        for b in QKV_BIASES:      # Q/K/V biases (fp32, never quantised); zero when absent
+            out[b] = _f64(src[b]) if b in src else 0.0
         out["attn_norm"] = _f64(src["attn_norm"])
         out["ffn_norm"] = _f64(src["ffn_norm"])
         if self._cache is not None:
@@ -224,10 +237,11 @@ class OracleModel:
 
 
 class OracleKV:
-    """Per-layer K and V (after RoPE for K) of every cached position, float64."""
+    """Per-layer K and V (after RoPE for K) of every cached position, float64,
+    [layer, position, K/V head, dim]."""
 
     def __init__(self, shape, capacity: int):
-        L, H, dh = shape.n_layers, shape.n_heads, shape.head_dim
+        L, H, dh = shape.n_layers, shape.kv_heads, shape.head_dim
         self.shape = shape
         self.capacity = capacity
         self.K = np.zeros((L, capacity, H, dh))
@@ -269,16 +283,16 @@ def forward_rows(model: OracleModel, kv: OracleKV, ids: np.ndarray, pos: np.ndar
     """
     sh = model.shape
     n = len(ids)
-    H, dh = sh.n_heads, sh.head_dim
+    H, Hkv, dh = sh.n_heads, sh.kv_heads, sh.head_dim
     pos = np.asarray(pos, dtype=np.int64)
     x = model.embed[np.asarray(ids, dtype=np.int64)].copy()
     n_layers = sh.n_layers if stop_layer is None else stop_layer
     for l in range(n_layers):
         w = model.layer(l)
         h = rmsnorm(x, w["attn_norm"], sh.eps)
-        q = (h @ w["wq"].T).reshape(n, H, dh)
-        k = (h @ w["wk"].T).reshape(n, H, dh)
-        v = (h @ w["wv"].T).reshape(n, H, dh)
+        q = (h @ w["wq"].T + w["bq"]).reshape(n, H, dh)
+        k = (h @ w["wk"].T + w["bk"]).reshape(n, Hkv, dh)
+        v = (h @ w["wv"].T + w["bv"]).reshape(n, Hkv, dh)
         q = rope(q, pos, sh.rope_base)
         k = rope(k, pos, sh.rope_base)
         kv.K[l, pos] = k
@@ -484,20 +498,20 @@ def block_causal_allowed(n_total: int, prompt_len: int, block: int, window_from:
 def forward_full(model: OracleModel, ids: np.ndarray, allowed: np.ndarray):
     """Recompute every row from scratch (no cache) under the boolean mask.
 
-    Returns (x [n, d], logits [n, V], K [L, n, H, Dh], V [L, n, H, Dh]).
+    Returns (x [n, d], logits [n, V], K [L, n, Hkv, Dh], V [L, n, Hkv, Dh]).
     """
     sh = model.shape
     n = len(ids)
-    H, dh = sh.n_heads, sh.head_dim
+    H, Hkv, dh = sh.n_heads, sh.kv_heads, sh.head_dim
     pos = np.arange(n)
     x = model.embed[np.asarray(ids, dtype=np.int64)].copy()
     Ks, Vs = [], []
     for l in range(sh.n_layers):
         w = model.layer(l)
         h = rmsnorm(x, w["attn_norm"], sh.eps)
-        q = rope((h @ w["wq"].T).reshape(n, H, dh), pos, sh.rope_base)
-        k = rope((h @ w["wk"].T).reshape(n, H, dh), pos, sh.rope_base)
-        v = (h @ w["wv"].T).reshape(n, H, dh)
+        q = rope((h @ w["wq"].T + w["bq"]).reshape(n, H, dh), pos, sh.rope_base)
+        k = rope((h @ w["wk"].T + w["bk"]).reshape(n, Hkv, dh), pos, sh.rope_base)
+        v = (h @ w["wv"].T + w["bv"]).reshape(n, Hkv, dh)
         Ks.append(k)
         Vs.append(v)
         o = attend_masked(q, k, v, allowed)

@@ -77,18 +77,29 @@ class Shape:
     eps: float = 1e-5
     rope_base: float = 10000.0
     block: int = 32
+    n_kv_heads: int = 0          # K/V heads (grouped-query attention); 0 = n_heads
+    qkv_bias: bool = False       # biases on the Q, K and V projections
 
     def __post_init__(self):
         assert self.n_heads * self.head_dim == self.d_model
         assert 0 <= self.mask_id < self.vocab
+        assert self.kv_heads >= 1 and self.n_heads % self.kv_heads == 0
 
     def with_layers(self, n_layers: int) -> "Shape":
         return dataclasses.replace(self, n_layers=n_layers)
 
     @property
+    def kv_heads(self) -> int:
+        return self.n_kv_heads or self.n_heads
+
+    @property
+    def d_kv(self) -> int:
+        return self.kv_heads * self.head_dim
+
+    @property
     def params_per_layer(self) -> int:
         d, f = self.d_model, self.d_ff
-        return 4 * d * d + 3 * f * d
+        return 2 * d * d + 2 * d * self.d_kv + 3 * f * d
 
 
 # Tiny fp32 model: 2 layers, d 256, 4 heads x 64, FFN 688, vocab 1024 (1023 = MASK).
@@ -103,21 +114,39 @@ LLADA_8B = Shape(n_layers=32, d_model=4096, n_heads=32, head_dim=128, d_ff=12288
 MICRO = Shape(n_layers=2, d_model=64, n_heads=2, head_dim=32, d_ff=96, vocab=80, mask_id=79)
 SMALL_BF16 = Shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ff=688, vocab=1000, mask_id=999)
 
-PRESETS = {"tiny": TINY, "llada8b": LLADA_8B, "micro": MICRO, "small": SMALL_BF16}
+# Dream-7B shape (grouped-query attention): 28 layers, d 3584, 28 query heads x 128
+# sharing 4 K/V heads, FFN 18944, vocab 152064, RoPE base 1e6, RMSNorm eps 1e-6,
+# biases on Q/K/V.  MASK = vocab - 1 as for the other shapes.
+DREAM_7B = Shape(n_layers=28, d_model=3584, n_heads=28, head_dim=128, d_ff=18944, vocab=152064, mask_id=152063,
+                 eps=1e-6, rope_base=1e6, n_kv_heads=4, qkv_bias=True)
+
+# Small grouped-query shapes: 2 query heads per K/V head (fp32 and bf16), and one
+# K/V head for 4 query heads (multi-query) with ragged FFN and vocab tiles.
+TINY_GQA = Shape(n_layers=2, d_model=256, n_heads=4, head_dim=64, d_ff=688, vocab=1024, mask_id=1023,
+                 n_kv_heads=2, qkv_bias=True)
+SMALL_MQA = Shape(n_layers=2, d_model=512, n_heads=4, head_dim=128, d_ff=688, vocab=1000, mask_id=999,
+                  n_kv_heads=1, qkv_bias=True)
+MICRO_GQA = Shape(n_layers=2, d_model=64, n_heads=4, head_dim=16, d_ff=96, vocab=80, mask_id=79, n_kv_heads=2,
+                  qkv_bias=True)
+
+PRESETS = {"tiny": TINY, "llada8b": LLADA_8B, "micro": MICRO, "small": SMALL_BF16, "dream7b": DREAM_7B,
+           "tiny_gqa": TINY_GQA, "small_mqa": SMALL_MQA}
 
 WEIGHT_STD = 0.02
 
 # Per-layer tensors in a fixed order; the index feeds the stream id.
 LAYER_TENSORS = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+LAYER_BIASES = ("bq", "bk", "bv")       # fp32 draws, present when shape.qkv_bias
 LAYER_GAINS = ("attn_norm", "ffn_norm")
 
 
 def tensor_shape(shape: Shape, name: str):
-    d, f, v = shape.d_model, shape.d_ff, shape.vocab
+    d, f, v, dkv = shape.d_model, shape.d_ff, shape.vocab, shape.d_kv
     return {
         "embed": (v, d), "lm_head": (v, d), "final_norm": (d,),
-        "wq": (d, d), "wk": (d, d), "wv": (d, d), "wo": (d, d),
+        "wq": (d, d), "wk": (dkv, d), "wv": (dkv, d), "wo": (d, d),
         "wg": (f, d), "wu": (f, d), "wd": (d, f),
+        "bq": (d,), "bk": (dkv,), "bv": (dkv,),
         "attn_norm": (d,), "ffn_norm": (d,),
     }[name]
 
@@ -127,7 +156,7 @@ def _stream_id(name: str, layer: int) -> int:
         return 1
     if name == "lm_head":
         return 2
-    return 1000 + 16 * layer + LAYER_TENSORS.index(name)
+    return 1000 + 16 * layer + (LAYER_TENSORS + LAYER_BIASES).index(name)
 
 
 def normal(seed: int, stream: int, n: int, dtype: str, offset: int = 0,
@@ -159,6 +188,9 @@ def weight(shape: Shape, name: str, layer: int = -1, dtype: str = "f32", seed: i
 
 def layer_weights(shape: Shape, layer: int, dtype: str = "f32", seed: int = 0) -> Dict[str, np.ndarray]:
     w = {n: weight(shape, n, layer, dtype, seed) for n in LAYER_TENSORS}
+    if shape.qkv_bias:
+        for b in LAYER_BIASES:
+            w[b] = weight(shape, b, layer, "f32", seed)
     for g in LAYER_GAINS:
         w[g] = weight(shape, g, layer)
     return w

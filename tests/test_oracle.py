@@ -5,6 +5,7 @@ library routine (PyTorch functional ops, SciPy softmax), or brute force on tiny
 inputs.  Together they are meant to catch a dropped term, a wrong sign or
 index, or a transposed operand anywhere in the oracle.
 """
+import dataclasses
 import itertools
 
 import numpy as np
@@ -35,6 +36,7 @@ def torch_forward(shape, w, ids, allowed):
     t = lambda a: torch.from_numpy(synth.as_f32(np.asarray(a))).double()
     n = len(ids)
     H, dh, d = shape.n_heads, shape.head_dim, shape.d_model
+    Hkv = shape.kv_heads
     half = dh // 2
     pos = torch.arange(n, dtype=torch.float64)
     inv = shape.rope_base ** (-torch.arange(half, dtype=torch.float64) * 2.0 / dh)
@@ -47,12 +49,13 @@ def torch_forward(shape, w, ids, allowed):
     x = t(w["embed"])[torch.as_tensor(np.asarray(ids, np.int64))]
     mask = torch.as_tensor(allowed)
     for lw in w["layers"]:
+        b = {k: (t(lw[k]) if k in lw else None) for k in ("bq", "bk", "bv")}
         h = F.rms_norm(x, (d,), weight=t(lw["attn_norm"]), eps=shape.eps)
-        q = rope_c(F.linear(h, t(lw["wq"])).view(n, H, dh))
-        k = rope_c(F.linear(h, t(lw["wk"])).view(n, H, dh))
-        v = F.linear(h, t(lw["wv"])).view(n, H, dh)
+        q = rope_c(F.linear(h, t(lw["wq"]), b["bq"]).view(n, H, dh))
+        k = rope_c(F.linear(h, t(lw["wk"]), b["bk"]).view(n, Hkv, dh))
+        v = F.linear(h, t(lw["wv"]), b["bv"]).view(n, Hkv, dh)
         o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
-                                           attn_mask=mask)
+                                           attn_mask=mask, enable_gqa=Hkv != H)
         x = x + F.linear(o.transpose(0, 1).reshape(n, d), t(lw["wo"]))
         h2 = F.rms_norm(x, (d,), weight=t(lw["ffn_norm"]), eps=shape.eps)
         x = x + F.linear(F.silu(F.linear(h2, t(lw["wg"]))) * F.linear(h2, t(lw["wu"])), t(lw["wd"]))
@@ -165,7 +168,8 @@ def test_planted_lm_head_row_forces_argmax():
 # ----------------------------------------------------------------------------
 
 
-@pytest.mark.parametrize("shape", [MICRO, synth.TINY.with_layers(1)], ids=["micro", "tiny1"])
+@pytest.mark.parametrize("shape", [MICRO, synth.TINY.with_layers(1), synth.MICRO_GQA,
+                                   synth.SMALL_MQA.with_layers(1)], ids=["micro", "tiny1", "micro_gqa", "small_mqa1"])
 def test_step_matches_torch_reference(shape):
     model, w = micro_model(shape)
     P0, W = 24, 12
@@ -199,6 +203,34 @@ def test_one_row_no_prefix_is_textbook_mlp_block():
     np.testing.assert_allclose(x[0], x2, rtol=1e-12, atol=1e-14)
 
 
+def test_gqa_equals_mha_with_each_kv_head_repeated():
+    """Grouped-query attention is multi-head attention whose K/V projections give
+    every query head of a group the same K/V head: repeating each K/V head's rows
+    (and biases) G times must reproduce the grouped model exactly."""
+    g = synth.MICRO_GQA
+    G = g.n_heads // g.kv_heads
+    m = dataclasses.replace(g, n_kv_heads=0)
+    model_g, w = micro_model(g)
+    wm = dict(w, layers=[])
+    for lw in w["layers"]:
+        lw2 = dict(lw)
+        for name in ("wk", "wv", "bk", "bv"):
+            a = lw[name].reshape(g.kv_heads, g.head_dim, *lw[name].shape[1:])
+            lw2[name] = np.repeat(a, G, axis=0).reshape(g.d_model, *lw[name].shape[1:])
+        wm["layers"].append(lw2)
+    model_m = oracle.OracleModel(m, wm)
+    P0, W = 24, 12
+    prompt = synth.prompt_ids(g, P0)
+    tok, mask = synth.window(g, W, range(3, W))
+    outs = []
+    for mod, sh in ((model_g, g), (model_m, m)):
+        kv = oracle.OracleKV(sh, P0 + W)
+        oracle.prefill(mod, kv, prompt)
+        outs.append(oracle.denoise_step(mod, kv, tok, mask))
+    fin = np.isfinite(outs[0].logits)
+    np.testing.assert_allclose(outs[0].logits[fin], outs[1].logits[fin], rtol=1e-12, atol=1e-13)
+
+
 # ----------------------------------------------------------------------------
 # Cache = brute-force recompute (block-causal), step = full forward
 # ----------------------------------------------------------------------------
@@ -216,8 +248,8 @@ def _build_prefix(model, sh, P0, n_blocks, cap):
     return kv, np.concatenate([prompt] + blocks)
 
 
-def test_cached_prefix_equals_block_causal_recompute():
-    sh = MICRO
+@pytest.mark.parametrize("sh", [MICRO, synth.MICRO_GQA], ids=["mha", "gqa"])
+def test_cached_prefix_equals_block_causal_recompute(sh):
     model, _ = micro_model(sh)
     P0 = 20
     kv, seq = _build_prefix(model, sh, P0, 2, P0 + 2 * sh.block)
