@@ -34,6 +34,9 @@ WORKLOADS = {
                                         masked=list(range(24, 64)), segs=[(0, 32, 4), (32, 32, 4)], sls=True),
     "llada8b_w8_p4096_w64_spec": dict(shape="llada8b", dtype="w8", prefix=4096, W=64,
                                       masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)], sls=True),
+    # Dream-7B (grouped-query attention, 28 query heads over 4 K/V heads, Q/K/V biases)
+    "dream7b_bf16_p512_w32": dict(shape="dream7b", dtype="bf16", prefix=512, W=32,
+                                  masked=list(range(8, 32)), segs=[(0, 32, 1)]),
 }
 DEFAULT = "llada8b_bf16_p512_w32"
 E2E = "llada8b_bf16_e2e128"      # end-to-end 128-token generation (prefill included)
@@ -559,7 +562,9 @@ def main():
             "measured_read_peak": round(read_gbs, 1), "frac_of_measured": round(dk["gbs"] / read_gbs, 4)}
 
     out = {
-        "metric": "denoising steps/sec + tokens/sec, LLaDA-8B shape, block 32; % of HBM roofline",
+        "metric": ("denoising steps/sec + tokens/sec, LLaDA-8B shape, block 32; % of HBM roofline"
+                   if wl["shape"] == "llada8b" else
+                   "denoising steps/sec + tokens/sec, Dream-7B shape, block 32; % of HBM roofline"),
         "value": round(steps_s, 2),
         "unit": "steps/s",
         "n_gpus": 1,
@@ -572,7 +577,8 @@ def main():
         "dtype": "bf16" if dtype == "bf16" else "int8w-bf16a",
         "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
         "config": {"workload": args.workload, "layers": shape.n_layers, "d_model": shape.d_model,
-                   "heads": shape.n_heads, "head_dim": shape.head_dim, "d_ff": shape.d_ff, "vocab": shape.vocab,
+                   "heads": shape.n_heads, "kv_heads": shape.kv_heads, "head_dim": shape.head_dim,
+                   "d_ff": shape.d_ff, "vocab": shape.vocab,
                    "prefix": P, "window": W, "masked": len(wl["masked"]), "commits_per_step": commits,
                    "lm_head_rows": n_need if sls else W},
         "query_tok_s": round(W * steps_s, 1),

@@ -15,7 +15,10 @@
  * Model: pre-norm LLaMA-style blocks (RMSNorm, multi-head attention with
  * rotate-half RoPE, SwiGLU FFN, no biases) and an untied LM head, as the paper's
  * operator list (RMSNorm, matrix multiplication, FlashAttention, elementwise ops;
- * Implementation section) and the LLaDA-8B model it evaluates imply.
+ * Implementation section) and the LLaDA-8B model it evaluates imply.  For the
+ * Dream-7B model of its cross-model study (Evaluation: grouped-query attention with
+ * fewer K/V heads) a config may give fewer K/V heads than query heads (query head h
+ * reads K/V head h / (n_heads / n_kv_heads)) and biases on the Q/K/V projections.
  *
  * Conventions
  *  - Every function returns an int status: DLLM_OK (0) or a negative DLLM_E_*.
@@ -82,11 +85,15 @@ typedef struct dllm_config {
     int32_t dtype;       /* DLLM_F32, DLLM_BF16 or DLLM_W8 */
     int32_t max_window;  /* largest row count of a step / append / refresh call (<= 256) */
     int32_t max_pos;     /* positions covered by the RoPE table; bounds every KV capacity */
+    int32_t n_kv_heads;  /* K/V heads (grouped-query attention); 0 = n_heads; must divide n_heads */
+    int32_t qkv_bias;    /* 1: the Q/K/V projections have fp32 biases (bq, bk, bv); else 0 */
 } dllm_config;
 
 /* Device pointers to row-major [out][in] matrices of one layer.
  * DLLM_F32: float; DLLM_BF16 and DLLM_W8: bfloat16 (W8 quantises them on create).
- * wq, wk, wv, wo: [d][d]; wg, wu: [d_ff][d]; wd: [d][d_ff]; norms: float [d]. */
+ * wq, wo: [d][d]; wk, wv: [dkv][d] with dkv = n_kv_heads * head_dim; wg, wu:
+ * [d_ff][d]; wd: [d][d_ff]; norms: float [d]; biases (read only when
+ * cfg.qkv_bias, else may be NULL): float bq [d], bk [dkv], bv [dkv]. */
 typedef struct dllm_layer_weights {
     const void* wq;
     const void* wk;
@@ -97,6 +104,9 @@ typedef struct dllm_layer_weights {
     const void* wd;
     const float* attn_norm;
     const float* ffn_norm;
+    const float* bq;
+    const float* bk;
+    const float* bv;
 } dllm_layer_weights;
 
 typedef struct dllm_weights {
@@ -126,7 +136,8 @@ int dllm_model_destroy(dllm_model* m);
 
 /* Bytes of device memory a KV cache of `capacity` positions needs (4 bytes per
  * cached value).  Layout inside the caller's buffer, with Cs = capacity rounded
- * up to a multiple of 32 and P = H*Cs*Dh elements per plane:
+ * up to a multiple of 32, H = n_kv_heads (n_heads if 0) and P = H*Cs*Dh elements
+ * per plane:
  *   F32 models, element float, 2 planes per layer (K, V^T):
  *     K   of layer l, head h, position p, dim j: (l*2+0)*P + (h*Cs + p)*Dh + j
  *     V^T of layer l, head h, dim j, position p: (l*2+1)*P + (h*Dh + j)*Cs + p

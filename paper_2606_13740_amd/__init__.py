@@ -32,11 +32,12 @@ class dllm_config(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("mask_id", ctypes.c_int32), ("block", ctypes.c_int32), ("eps", ctypes.c_float),
                 ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32), ("max_window", ctypes.c_int32),
-                ("max_pos", ctypes.c_int32)]
+                ("max_pos", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("qkv_bias", ctypes.c_int32)]
 
 
 class dllm_layer_weights(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm", "ffn_norm")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm", "ffn_norm",
+                                               "bq", "bk", "bv")]
 
 
 class dllm_weights(ctypes.Structure):
@@ -260,7 +261,8 @@ DTYPES = {"f32": DLLM_F32, "bf16": DLLM_BF16, "w8": DLLM_W8}
 
 def make_config(shape, dtype: str, max_window: int = 64, max_pos: int = 8192) -> dllm_config:
     return dllm_config(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ff, shape.vocab,
-                       shape.mask_id, shape.block, shape.eps, shape.rope_base, DTYPES[dtype], max_window, max_pos)
+                       shape.mask_id, shape.block, shape.eps, shape.rope_base, DTYPES[dtype], max_window, max_pos,
+                       getattr(shape, "n_kv_heads", 0), int(getattr(shape, "qkv_bias", False)))
 
 
 class Model:
@@ -294,8 +296,9 @@ class Model:
             src = layer_source(l)
             t = {k: up(v) for k, v in src.items()}
             keep.append(t)
-            layers[l] = dllm_layer_weights(*[t[k].data_ptr() for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd",
-                                                                      "attn_norm", "ffn_norm")])
+            layers[l] = dllm_layer_weights(*[t[k].data_ptr() if k in t else None
+                                             for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm",
+                                                       "ffn_norm", "bq", "bk", "bv")])
         g = {k: up(v) for k, v in globals_.items()}
         keep.append(g)
         w = dllm_weights(g["embed"].data_ptr(), g["lm_head"].data_ptr(), g["final_norm"].data_ptr(), layers)
@@ -333,7 +336,7 @@ class KVCache:
         return (self.capacity + 31) // 32 * 32
 
     def views(self):
-        """(K [L][H][Cs][Dh], V^T [L][H][Dh][Cs]) as float32 tensors.
+        """(K [L][Hkv][Cs][Dh], V^T [L][Hkv][Dh][Cs]) as float32 tensors (Hkv K/V heads).
 
         fp32 models: views of the buffer.  bf16 / int8 models: hi + lo of the two
         bf16 planes (a new tensor, not a view)."""
@@ -341,7 +344,8 @@ class KVCache:
 
         sh = self.model.shape
         Cs = self.row_stride
-        plane = sh.n_heads * Cs * sh.head_dim
+        Hkv = getattr(sh, "kv_heads", sh.n_heads)
+        plane = Hkv * Cs * sh.head_dim
         if self.model.dtype == "f32":
             flat = self.buf.view(torch.uint8)[: sh.n_layers * 2 * plane * 4].view(torch.float32)
             per = flat.view(sh.n_layers, 2, plane)
@@ -350,8 +354,8 @@ class KVCache:
             flat = self.buf.view(torch.uint8)[: sh.n_layers * 4 * plane * 2].view(torch.bfloat16)
             per = flat.view(sh.n_layers, 4, plane).float()
             K, Vt = per[:, 0] + per[:, 1], per[:, 2] + per[:, 3]
-        return (K.reshape(sh.n_layers, sh.n_heads, Cs, sh.head_dim),
-                Vt.reshape(sh.n_layers, sh.n_heads, sh.head_dim, Cs))
+        return (K.reshape(sh.n_layers, Hkv, Cs, sh.head_dim),
+                Vt.reshape(sh.n_layers, Hkv, sh.head_dim, Cs))
 
     @property
     def prefix_len(self) -> int:

@@ -21,11 +21,12 @@ namespace dllm {
 struct AttnArgs {
     const void* q;        // [rows][H][Dh]
     size_t q_plane;       // elements from the hi to the lo plane of q (bf16 path)
-    const void* K;        // layer base [H][Cs][Dh]
-    const void* Vt;       // layer base [H][Dh][Cs]
+    const void* K;        // layer base [Hkv][Cs][Dh]
+    const void* Vt;       // layer base [Hkv][Dh][Cs]
     size_t kv_plane;      // elements from the hi to the lo plane of K and V^T (bf16 path)
     int Cs;               // cache row stride (multiple of 32)
-    int H;
+    int H;                // query heads
+    int G;                // query heads per K/V head (grouped-query attention; 1 = multi-head)
     int T;                // keys [0, T) for rows without their own limit
     const int* lim;       // per-row key limit (rows < M) or nullptr
     int M;                // real rows
@@ -76,8 +77,9 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
     const float sl2 = a.scale * 1.4426950408889634f;
 
     const uint16_t* qp = (const uint16_t*)a.q;
-    const uint16_t* Kp = (const uint16_t*)a.K + (size_t)h * a.Cs * DH;
-    const uint16_t* Vp = (const uint16_t*)a.Vt + (size_t)h * DH * a.Cs;
+    const int hk = h / a.G;                                  // K/V head of this query head
+    const uint16_t* Kp = (const uint16_t*)a.K + (size_t)hk * a.Cs * DH;
+    const uint16_t* Vp = (const uint16_t*)a.Vt + (size_t)hk * DH * a.Cs;
 
     const int nblk = (a.T + 31) >> 5;
     const int kb0 = split * a.bps, kb1 = min(nblk, kb0 + a.bps);
@@ -281,8 +283,9 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
     const int row = blockIdx.x, h = blockIdx.y;
     const int ld = a.H * DH;
     const float* qp = (const float*)a.q + (size_t)row * ld + h * DH;
-    const float* Kp = (const float*)a.K + (size_t)h * a.Cs * DH;
-    const float* Vp = (const float*)a.Vt + (size_t)h * DH * a.Cs;
+    const int hk = h / a.G;                                  // K/V head of this query head
+    const float* Kp = (const float*)a.K + (size_t)hk * a.Cs * DH;
+    const float* Vp = (const float*)a.Vt + (size_t)hk * DH * a.Cs;
     const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
 
     float q[DH];

@@ -57,6 +57,7 @@ struct LayerW {
     PackedW qkv, o, gu, down;
     float* g1 = nullptr;
     float* g2 = nullptr;
+    float* bqkv = nullptr;   // Q/K/V biases in packed-row order, or nullptr
 };
 
 struct Workspace {
@@ -93,6 +94,7 @@ struct dllm_model {
     bool xf32 = false;       // activations in fp32
     size_t kv_elem = 4;      // bytes per cached K or V value (fp32, or a bf16 hi/lo pair)
     int KCx_d = 0, KCx_f = 0;
+    int Hkv = 0, dkv = 0;    // K/V heads and K (or V) rows per layer
     std::vector<LayerW> layers;
     PackedW lm;
     void* embed = nullptr;
@@ -101,6 +103,7 @@ struct dllm_model {
     void* wpool = nullptr;   // packed weights of every matrix
     float* spool = nullptr;  // int8 scales
     float* gpool = nullptr;  // norm gains
+    float* bpool = nullptr;  // Q/K/V biases
     Workspace ws;
     int n_lm_wg = 1;
     // probe
@@ -141,24 +144,50 @@ int pick_MT(int M) {
 //   gate/up 6 row tiles per workgroup, K split over 8 waves         (5.2 TB/s)
 //   LM head 4 waves x 8 row tiles, each wave streams the whole K    (6.3 TB/s)
 //   O/down 4 row tiles, K split over 8 waves x 4 workgroups (split-K) + reduction
-// Small models (fewer row tiles than CUs x tiles) use one tile per workgroup.
-bool big(GemmKind k, int n_tiles) {
-    switch (k) {
-        case G_QKV: return n_tiles >= 256 * 3;
-        case G_GU: return n_tiles >= 256 * 6;
-        case G_LM: return n_tiles >= 256 * 8;
-        default: return n_tiles >= 256;
+// These are template shapes; a launch may give each wave group fewer row tiles
+// (tpg) and fewer split-K slices (ks).  Every workgroup of these layouts holds a
+// whole CU (8 waves at ~200 VGPRs, or 100+ KiB of LDS), so a launch of more than
+// 256 workgroups runs in rounds: (tpg, ks) is chosen to minimise the busiest CU's
+// share, rounds x tpg / ks row tiles of full K, which picks the layouts above at
+// the LLaDA-8B widths (256 or 247 workgroups) and e.g. 5 tiles per wave group for
+// the Dream-7B gate/up and LM head.  Small models (fewer row tiles than the
+// thresholds below) use one tile per 4-wave workgroup.
+struct Decomp {
+    bool small;   // 1 tile per workgroup of 4 waves, K over the waves
+    int tpg;      // row tiles per wave group
+    int ks;       // split-K slices (residual projections)
+};
+
+constexpr int N_CU = 256;
+
+int template_fw(GemmKind k) { return k == G_QKV ? 3 : (k == G_GU ? 6 : (k == G_LM ? 8 : 4)); }
+int template_nwn(GemmKind k) { return k == G_LM ? 4 : 1; }
+
+Decomp decomp(GemmKind k, int n_tiles, int Mc, int gy) {
+    const int min_tiles = (k == G_QKV || k == G_RES) ? 128 : (k == G_GU ? 256 : 512);
+    if (n_tiles < min_tiles) return Decomp{true, 1, 1};
+    const int fw = template_fw(k), nwn = template_nwn(k);
+    Decomp best{false, 1, 1};
+    double best_load = 1e30;
+    for (int tpg = fw; tpg >= 1; --tpg) {
+        for (int ks = (k == G_RES && Mc <= 64) ? RES_SPLIT : 1; ks >= 1; ks >>= 1) {
+            const long wgs = (long)ceil_div(ceil_div(n_tiles, tpg), nwn) * ks * gy;
+            const double load = (double)ceil_div(wgs, N_CU) * tpg / ks;
+            if (load < best_load - 1e-9) { best_load = load; best = Decomp{false, tpg, ks}; }
+        }
     }
+    return best;
 }
 
 template <int WT, int FW, int NWn, int NWk, int MT, class Epi>
 void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
-    dim3 grid(ceil_div(n_tiles, FW * NWn), KS, gy);
+    dim3 grid(ceil_div(ceil_div(n_tiles, g.tpg), NWn), KS, gy);
     hipLaunchKernelGGL((gemm_kernel<WT, FW, NWn, NWk, MT, Epi>), grid, dim3(NWn * NWk * 64), 0, s, g, epi);
 }
 
 template <int WT, int FW, int NWn, int NWk, class Epi>
 int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
+    if (g.tpg < 1 || g.tpg > FW) return fail(DLLM_E_INVAL, "internal: row tiles per group outside the template");
     switch (MT) {
         case 1: launch_gemm_inst<WT, FW, NWn, NWk, 1>(g, epi, n_tiles, KS, gy, s); break;
         case 2: launch_gemm_inst<WT, FW, NWn, NWk, 2>(g, epi, n_tiles, KS, gy, s); break;
@@ -169,32 +198,18 @@ int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int K
     return DLLM_OK;
 }
 
-// Number of row groups (partials) a launch writes.
-int row_groups(GemmKind k, int n_tiles) {
-    switch (k) {
-        case G_QKV: return big(k, n_tiles) ? ceil_div(n_tiles, 3) : n_tiles;
-        case G_GU: return big(k, n_tiles) ? ceil_div(n_tiles, 6) : n_tiles;
-        case G_LM: return big(k, n_tiles) ? ceil_div(n_tiles, 8) : n_tiles;
-        default: return big(k, n_tiles) ? ceil_div(n_tiles, 4) : n_tiles;
-    }
-}
+// Number of row groups (LM-head partial records) a launch writes.
+int row_groups(const Decomp& dc, int n_tiles) { return ceil_div(n_tiles, dc.tpg); }
 
 template <int WT, GemmKind KIND, class Epi>
-int launch_gemm(int n_tiles, int MT, int KS, const GemmArgs& g, const Epi& epi, int gy, hipStream_t s) {
-    const bool b = big(KIND, n_tiles);
-    if constexpr (KIND == G_QKV) {
-        if (b) return launch_gemm_mt<WT, 3, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
-    } else if constexpr (KIND == G_GU) {
-        if (b) return launch_gemm_mt<WT, 6, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
-    } else if constexpr (KIND == G_LM) {
-        if (b) return launch_gemm_mt<WT, 8, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, 1, gy, s);
-    } else {
-        if (b) return launch_gemm_mt<WT, 4, 1, 8>(MT, g, epi, n_tiles, KS, gy, s);
-        return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, KS, gy, s);
-    }
+int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const Epi& epi, int gy, hipStream_t s) {
+    GemmArgs g = g0;
+    g.tpg = dc.tpg;
+    if (dc.small) return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, dc.ks, gy, s);
+    if constexpr (KIND == G_QKV) return launch_gemm_mt<WT, 3, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
+    else if constexpr (KIND == G_GU) return launch_gemm_mt<WT, 6, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
+    else if constexpr (KIND == G_LM) return launch_gemm_mt<WT, 8, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
+    else return launch_gemm_mt<WT, 4, 1, 8>(MT, g, epi, n_tiles, dc.ks, gy, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -328,6 +343,9 @@ int validate_config(const dllm_config* c) {
     if (c->d_model % 32 != 0) return fail(DLLM_E_DTYPE, "d_model must be a multiple of 32");
     if (c->d_model > 4 * ROW_NT * ROW_VPT) return fail(DLLM_E_DTYPE, "d_model must be <= 8192");
     if (c->d_ff % 8 != 0) return fail(DLLM_E_DTYPE, "d_ff must be a multiple of 8");
+    if (c->n_kv_heads < 0 || c->n_kv_heads > c->n_heads || (c->n_kv_heads > 0 && c->n_heads % c->n_kv_heads != 0))
+        return fail(DLLM_E_INVAL, "n_kv_heads must be 0 or divide n_heads");
+    if (c->qkv_bias != 0 && c->qkv_bias != 1) return fail(DLLM_E_INVAL, "qkv_bias must be 0 or 1");
     return DLLM_OK;
 }
 
@@ -361,11 +379,12 @@ int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* g
                   hipStream_t s, bool sel = false, const uint8_t* need = nullptr, int n_sel = 0) {
     Workspace& w = m->ws;
     const int d = m->cfg.d_model;
-    const int KS = (Mc <= 64 && big(G_RES, W.n_tiles)) ? RES_SPLIT : 1;
+    const Decomp dc = decomp(G_RES, W.n_tiles, Mc, gy);
+    const int KS = dc.ks;
     if ((size_t)KS * Mc * d > w.part_floats) return fail(DLLM_E_INVAL, "internal: split-K buffer too small");
     GemmArgs g{W.w, W.scale, X, W.KCw, W.KCw * WTraits<WT>::XPER, W.n_tiles};
     EpiPartial e{w.part, d, Mc};
-    int rc = launch_gemm<WT, G_RES>(W.n_tiles, MT, KS, g, e, gy, s);
+    int rc = launch_gemm<WT, G_RES>(dc, W.n_tiles, MT, g, e, gy, s);
     if (rc) return rc;
     hipLaunchKernelGGL((residual_reduce_kernel<XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const float*)w.part, KS, Mc, d,
                        M, m->cfg.eps, w.x, gnext, w.xg, m->KCx_d, sel, need, n_sel);
@@ -397,8 +416,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const AT*)m->embed, a.tok, a.mask,
                        a.M, d, c.vocab, c.mask_id, c.eps, (const float*)m->layers[0].g1, w.x, w.xg, m->KCx_d);
 
-    // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo].
-    const size_t plane = (size_t)H * kv->Cs * Dh;
+    // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo]; Hkv heads.
+    const size_t plane = (size_t)m->Hkv * kv->Cs * Dh;
     const size_t layer_elems = (XF32 ? 2 : 4) * plane;
     const size_t kv_plane = XF32 ? 0 : plane;
     const size_t q_plane = XF32 ? 0 : (size_t)w.rows * d;
@@ -409,15 +428,18 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
 
         // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
         {
-            GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles};
-            EpiQKV<XF32> e{d, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane, kv->Cs};
+            GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles, L.bqkv};
+            EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane,
+                           kv->Cs};
             ProbeScope ps(m, DLLM_K_QKV, s);
-            if ((rc = launch_gemm<WT, G_QKV>(L.qkv.n_tiles, MT, 1, g, e, gy, s))) return rc;
+            if ((rc = launch_gemm<WT, G_QKV>(decomp(G_QKV, L.qkv.n_tiles, Mc, gy), L.qkv.n_tiles, MT, g, e, gy, s)))
+                return rc;
         }
         // attention over [0, T) (+ split merge)
         {
             AttnArgs at{};
-            at.q = w.q; at.q_plane = q_plane; at.K = Kc; at.Vt = Vt; at.kv_plane = kv_plane; at.Cs = kv->Cs; at.H = H; at.T = a.T; at.lim = a.lim; at.M = a.M;
+            at.q = w.q; at.q_plane = q_plane; at.K = Kc; at.Vt = Vt; at.kv_plane = kv_plane; at.Cs = kv->Cs; at.H = H;
+            at.G = H / m->Hkv; at.T = a.T; at.lim = a.lim; at.M = a.M;
             at.scale = 1.0f / sqrtf((float)Dh); at.o = w.of; at.KCx = m->KCx_d;
             at.opart = w.opart; at.mlpart = w.mlpart; at.rows_ld = w.wrows;
             ProbeScope ps(m, DLLM_K_ATTN, s);
@@ -462,7 +484,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
             GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles};
             EpiSwiGLU<XF32> e{w.af, m->KCx_f};
             ProbeScope ps(m, DLLM_K_GATEUP, s);
-            if ((rc = launch_gemm<WT, G_GU>(L.gu.n_tiles, MT, 1, g, e, gy, s))) return rc;
+            if ((rc = launch_gemm<WT, G_GU>(decomp(G_GU, L.gu.n_tiles, Mc, gy), L.gu.n_tiles, MT, g, e, gy, s)))
+                return rc;
         }
         // down projection + residual (+ next norm operand)
         {
@@ -485,11 +508,13 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         }
         if (gyl * MTl * 16 > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
         GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles};
-        const int gx = row_groups(G_LM, m->lm.n_tiles);
+        const Decomp dc = decomp(G_LM, m->lm.n_tiles, gyl * MTl * 16, gyl);
+        const int gx = row_groups(dc, m->lm.n_tiles);
+        if (gx > m->n_lm_wg) return fail(DLLM_E_INVAL, "internal: LM-head partials exceed their buffer");
         if (Ml > 0) {
             EpiLM e{c.vocab, c.mask_id, Ml, w.lm, w.wrows, a.logits};
             ProbeScope ps(m, DLLM_K_LMHEAD, s);
-            if ((rc = launch_gemm<WT, G_LM>(m->lm.n_tiles, MTl, 1, g, e, gyl, s))) return rc;
+            if ((rc = launch_gemm<WT, G_LM>(dc, m->lm.n_tiles, MTl, g, e, gyl, s))) return rc;
         }
         hipLaunchKernelGGL(lm_combine_kernel, dim3(a.M), dim3(64), 0, s, (const LmPartial*)w.lm, gx, w.wrows,
                            a.out_id, a.out_conf, a.sel, a.need, a.n_sel, a.M);
@@ -534,6 +559,8 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
         const dllm_layer_weights& L = w->layers[l];
         if (!L.wq || !L.wk || !L.wv || !L.wo || !L.wg || !L.wu || !L.wd || !L.attn_norm || !L.ffn_norm)
             return fail(DLLM_E_INVAL, "weights: NULL pointer in layer " + std::to_string(l));
+        if (cfg->qkv_bias && (!L.bq || !L.bk || !L.bv))
+            return fail(DLLM_E_INVAL, "weights: NULL bias pointer in layer " + std::to_string(l));
     }
     hipStream_t s = (hipStream_t)stream;
     dllm_model* m = new dllm_model();
@@ -542,6 +569,8 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     m->wt = c.dtype == DLLM_F32 ? WT_F32 : (c.dtype == DLLM_BF16 ? WT_BF16 : WT_I8);
     m->xf32 = c.dtype == DLLM_F32;
     m->kv_elem = 4;
+    m->Hkv = c.n_kv_heads > 0 ? c.n_kv_heads : c.n_heads;
+    m->dkv = m->Hkv * c.head_dim;
     const int xcols = m->xf32 ? 16 : 32;
     const int xper = m->wt == WT_I8 ? 2 : 1;
     const int d = c.d_model, F = c.d_ff;
@@ -549,7 +578,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     m->layers.resize(c.n_layers);
     size_t wbytes = 0, srows = 0;
     for (auto& L : m->layers) {
-        plan_packed(L.qkv, m->wt, 3 * d, d);
+        plan_packed(L.qkv, m->wt, d + 2 * m->dkv, d);
         plan_packed(L.o, m->wt, d, d);
         plan_packed(L.gu, m->wt, 2 * F, d);
         plan_packed(L.down, m->wt, d, F);
@@ -561,7 +590,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     m->KCx_d = m->layers[0].qkv.KCw * xper;
     m->KCx_f = m->layers[0].down.KCw * xper;
     (void)xcols;
-    m->n_lm_wg = row_groups(G_LM, m->lm.n_tiles);
+    m->n_lm_wg = m->lm.n_tiles;   // row groups of any LM-head launch (at least one tile each)
 
     auto cleanup = [&](int code) {
         dllm_model_destroy(m);
@@ -570,6 +599,8 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     if ((rc = alloc_zero(&m->wpool, wbytes))) return cleanup(rc);
     if (m->wt == WT_I8 && (rc = alloc_zero((void**)&m->spool, srows * 4))) return cleanup(rc);
     if ((rc = alloc_zero((void**)&m->gpool, (size_t)(2 * c.n_layers + 1) * d * 4))) return cleanup(rc);
+    const int qkv_rows = m->layers[0].qkv.n_tiles * 16;     // packed (padded) Q/K/V rows
+    if (c.qkv_bias && (rc = alloc_zero((void**)&m->bpool, (size_t)c.n_layers * qkv_rows * 4))) return cleanup(rc);
     const size_t esize = m->xf32 ? 4 : 2;
     if ((rc = alloc_zero(&m->embed, (size_t)c.vocab * d * esize))) return cleanup(rc);
     const int half = c.head_dim / 2;
@@ -588,19 +619,24 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     for (int l = 0; l < c.n_layers; ++l) {
         m->layers[l].g1 = m->gpool + (size_t)(2 * l) * d;
         m->layers[l].g2 = m->gpool + (size_t)(2 * l + 1) * d;
+        if (m->bpool) m->layers[l].bqkv = m->bpool + (size_t)l * qkv_rows;
     }
     m->gf = m->gpool + (size_t)(2 * c.n_layers) * d;
 
     // pack
     const bool src_f32 = (c.dtype == DLLM_F32);
     auto pack = [&](PackedW& p, int kind, const void* a0, const void* a1, const void* a2) -> int {
-        PackSrc src{{a0, a1, a2}, kind, p.N, p.K, d, c.head_dim};
+        PackSrc src{{a0, a1, a2}, kind, p.N, p.K, d, c.head_dim, m->dkv};
         return src_f32 ? pack_one<float>(m, p, src, s) : pack_one<uint16_t>(m, p, src, s);
     };
     for (int l = 0; l < c.n_layers; ++l) {
         const dllm_layer_weights& S = w->layers[l];
         LayerW& L = m->layers[l];
         if ((rc = pack(L.qkv, MAP_QKV, S.wq, S.wk, S.wv))) return cleanup(rc);
+        if (L.bqkv) {
+            PackSrc bs{{S.bq, S.bk, S.bv}, MAP_QKV, L.qkv.N, 1, d, c.head_dim, m->dkv};
+            hipLaunchKernelGGL(pack_bias_kernel, dim3(ceil_div(qkv_rows, 256)), dim3(256), 0, s, bs, qkv_rows, L.bqkv);
+        }
         if ((rc = pack(L.o, MAP_IDENT, S.wo, nullptr, nullptr))) return cleanup(rc);
         if ((rc = pack(L.gu, MAP_GATEUP, S.wg, S.wu, nullptr))) return cleanup(rc);
         if ((rc = pack(L.down, MAP_IDENT, S.wd, nullptr, nullptr))) return cleanup(rc);
@@ -627,7 +663,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
 int dllm_model_destroy(dllm_model* m) {
     if (!m) return DLLM_OK;
     free_ws(m->ws);
-    void* ptrs[] = {m->wpool, m->spool, m->gpool, m->embed, m->rope};
+    void* ptrs[] = {m->wpool, m->spool, m->gpool, m->bpool, m->embed, m->rope};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     for (auto e : m->ev_b) (void)hipEventDestroy(e);
@@ -643,7 +679,7 @@ int dllm_kv_bytes(const dllm_model* m, int32_t capacity, size_t* bytes) {
     if (capacity < 1 || capacity > m->cfg.max_pos)
         return fail(DLLM_E_CAPACITY, "capacity must be in [1, max_pos]");
     const dllm_config& c = m->cfg;
-    *bytes = (size_t)c.n_layers * 2 * c.n_heads * cs_of(capacity) * c.head_dim * m->kv_elem;
+    *bytes = (size_t)c.n_layers * 2 * m->Hkv * cs_of(capacity) * c.head_dim * m->kv_elem;
     return DLLM_OK;
 }
 
@@ -914,12 +950,15 @@ int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int3
     const dllm_config& c = m->cfg;
     const double wsz = m->wt == WT_F32 ? 4.0 : (m->wt == WT_BF16 ? 2.0 : 1.0);
     const double asz = (double)m->kv_elem;   // activations and cache values: 4 bytes
-    const double d = c.d_model, F = c.d_ff, V = c.vocab;
+    const double d = c.d_model, F = c.d_ff, V = c.vocab, dkv = m->dkv;
     const double scale_b = (m->wt == WT_I8) ? 4.0 : 0.0;   // per weight row
+    const double bias_b = c.qkv_bias ? 4.0 : 0.0;           // per Q/K/V row
     double b = 0;
     switch (kernel_class) {
-        case DLLM_K_QKV: b = 3 * d * d * wsz + 3 * d * scale_b + W * d * asz + 2.0 * W * d * asz + W * d * asz; break;
-        case DLLM_K_ATTN: b = 2.0 * (P + W) * d * asz + 2.0 * W * d * asz; break;
+        case DLLM_K_QKV:
+            b = (d + 2 * dkv) * (d * wsz + scale_b + bias_b) + W * d * asz + 2.0 * W * dkv * asz + W * d * asz;
+            break;
+        case DLLM_K_ATTN: b = 2.0 * (P + W) * dkv * asz + 2.0 * W * d * asz; break;
         case DLLM_K_OPROJ: b = d * d * wsz + d * scale_b + W * d * asz + 2.0 * W * d * 4 + W * d * asz; break;
         case DLLM_K_GATEUP: b = 2 * F * d * wsz + 2 * F * scale_b + W * d * asz + W * F * asz; break;
         case DLLM_K_DOWN: b = d * F * wsz + d * scale_b + W * F * asz + 2.0 * W * d * 4 + W * d * asz; break;

@@ -10,8 +10,9 @@
 // projection feeds (RoPE + KV write, residual, SwiGLU, LM-head reduction).
 //
 // Row scales (int8 weights) multiply Y per weight row (they factor out of the K
-// sum).  The A operand arrives already normalised (RMSNorm applied by the
-// kernel that finished the residual row).
+// sum), and row biases (Q/K/V projections) are added after them.  The A operand
+// arrives already normalised (RMSNorm applied by the kernel that finished the
+// residual row).
 #pragma once
 
 #include <type_traits>
@@ -27,6 +28,8 @@ struct GemmArgs {
     int KCw;              // weight chunks per row tile
     int KCx;              // activation chunks per token tile
     int n_tiles;          // packed rows / 16
+    const float* bias = nullptr;  // per packed row (added after the row scale) or nullptr
+    int tpg = 0;          // row tiles per wave group (1 .. FW); the launch sets it
 };
 
 // Epilogue interface:
@@ -60,8 +63,8 @@ constexpr int reduce_slots(int slot_bytes) {
     return s;
 }
 
-// Workgroup layout: NWn x NWk waves.  Wave (wn, wk) streams FW row tiles (group
-// wn) over slice wk of the workgroup's K range; the NWk slices of a group are
+// Workgroup layout: NWn x NWk waves.  Wave (wn, wk) streams g.tpg <= FW row tiles
+// (group wn) over slice wk of the workgroup's K range; the NWk slices of a group are
 // summed in LDS in a fixed order.  grid = (row groups / NWn, KS, token blocks):
 // blockIdx.y picks one of KS contiguous K ranges (split-K; the partial results
 // go to an epilogue that stores them for a separate reduction).
@@ -96,15 +99,15 @@ gemm_kernel(GemmArgs g, Epi epi) {
     typename Epi::Pre pre[NWn];
 #pragma unroll
     for (int q = 0; q < NWn; ++q) {
-        const int nq0 = (blockIdx.x * NWn + q) * FW;
-        const int nfq = max(0, min(FW, g.n_tiles - nq0));
+        const int nq0 = (blockIdx.x * NWn + q) * g.tpg;
+        const int nfq = max(0, min(g.tpg, g.n_tiles - nq0));
         if (nfq > 0) epi.fetch(pre[q], nq0 * 16, nfq * 16, mt0 * 16, MR);
     }
     auto stage_prologue = [&]() {
 #pragma unroll
         for (int q = 0; q < NWn; ++q) {
-            const int nq0 = (blockIdx.x * NWn + q) * FW;
-            const int nfq = max(0, min(FW, g.n_tiles - nq0));
+            const int nq0 = (blockIdx.x * NWn + q) * g.tpg;
+            const int nfq = max(0, min(g.tpg, g.n_tiles - nq0));
             if (nfq > 0) epi.stage(pre[q], esm + q * ESM, nq0 * 16, nfq * 16, mt0 * 16, MR);
         }
     };
@@ -116,8 +119,8 @@ gemm_kernel(GemmArgs g, Epi epi) {
         for (int t = 0; t < MT; ++t) acc[f][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     {
-        const int nt0 = (blockIdx.x * NWn + wn) * FW;
-        const int nf = max(0, min(FW, g.n_tiles - nt0));
+        const int nt0 = (blockIdx.x * NWn + wn) * g.tpg;
+        const int nf = max(0, min(g.tpg, g.n_tiles - nt0));
         const unsigned span = (unsigned)(kb1 - kb0);
         const int c0 = kb0 + (int)(((unsigned)wk * span) / NWk);
         const int c1 = kb0 + (int)(((unsigned)(wk + 1) * span) / NWk);
@@ -222,15 +225,18 @@ gemm_kernel(GemmArgs g, Epi epi) {
         __syncthreads();
     }
 
-    // Row scales (int8), then the epilogue of each row group.
+    // Row scales (int8) and biases, then the epilogue of each row group.
     for (int q = 0; q < NWn; ++q) {
-        const int nt0 = (blockIdx.x * NWn + q) * FW;
-        const int nf = max(0, min(FW, g.n_tiles - nt0));
+        const int nt0 = (blockIdx.x * NWn + q) * g.tpg;
+        const int nf = max(0, min(g.tpg, g.n_tiles - nt0));
         if (nf == 0) break;
-        if (g.wscale != nullptr) {
+        if (g.wscale != nullptr || g.bias != nullptr) {
             for (int idx = threadIdx.x; idx < NR * MR; idx += blockDim.x) {
                 const int n = idx / MR, m = idx % MR;
-                Y[q][n * LDY + m] *= g.wscale[nt0 * 16 + n];
+                float y = Y[q][n * LDY + m];
+                if (g.wscale != nullptr) y *= g.wscale[nt0 * 16 + n];
+                if (g.bias != nullptr) y += g.bias[nt0 * 16 + n];
+                Y[q][n * LDY + m] = y;
             }
             __syncthreads();
         }
@@ -251,14 +257,14 @@ gemm_kernel(GemmArgs g, Epi epi) {
 template <bool XF32>
 struct EpiQKV {
     using T = typename std::conditional<XF32, float, uint16_t>::type;
-    int d, Dh, M;
+    int d, dkv, Dh, M;      // Q rows (H * Dh), K and V rows each (Hkv * Dh), head size, real tokens
     int pos_base;           // position of token m is pos ? pos[m] : pos_base + m
     const int* pos;
     const float2* rope;     // [max_pos][Dh/2] (cos, sin)
     T* q;                   // [rows][d] (+ lo plane at q + q_plane)
     size_t q_plane;
-    T* Kc;                  // layer base of K   [H][Cs][Dh] (+ lo plane at kv_plane)
-    T* Vt;                  // layer base of V^T [H][Dh][Cs] (+ lo plane at kv_plane)
+    T* Kc;                  // layer base of K   [Hkv][Cs][Dh] (+ lo plane at kv_plane)
+    T* Vt;                  // layer base of V^T [Hkv][Dh][Cs] (+ lo plane at kv_plane)
     size_t kv_plane;
     int Cs;
 
@@ -286,8 +292,8 @@ struct EpiQKV {
     __device__ __forceinline__ bool rope_entry(int idx, int n0, int npairs, int m0, float2& v) const {
         const int p = idx % npairs, ml = idx / npairs;
         const int m = m0 + ml, n = n0 + 2 * p;
-        if (m >= M || n >= 2 * d) return false;
-        const int rr = (n % d) % Dh;
+        if (m >= M || n >= d + dkv) return false;
+        const int rr = n % Dh;                       // d is a multiple of Dh
         const int ps = pos ? pos[m] : pos_base + m;
         v = rope[(size_t)ps * (Dh >> 1) + (rr >> 1)];
         return true;
@@ -335,7 +341,7 @@ struct EpiQKV {
         const int half = Dh >> 1;
         const bool staged = npairs * mcols <= kPairs;
         const float2* csm = (const float2*)sm;
-        if (n0 + nrows <= 2 * d) {
+        if (n0 + nrows <= d + dkv) {
             // Q / K rows: four consecutive RoPE pairs (dims j..j+3 and j+half..j+half+3) per thread
             const int nq = npairs >> 2;
             for (int idx = threadIdx.x; idx < nq * mcols; idx += blockDim.x) {
@@ -344,7 +350,7 @@ struct EpiQKV {
                 if (m >= M) continue;
                 const int p0 = 4 * qd, n = n0 + 2 * p0;
                 const int ps = pos ? pos[m] : pos_base + m;
-                const int seg = n / d, nn = n - seg * d;
+                const int seg = n < d ? 0 : 1, nn = n - seg * d;
                 const int h = nn / Dh, j0 = (nn - h * Dh) >> 1;
                 float ra[4], rb[4];
 #pragma unroll
@@ -361,7 +367,7 @@ struct EpiQKV {
             }
             return;
         }
-        if (n0 >= 2 * d && pos == nullptr && ((pos_base + m0) & 3) == 0) {
+        if (n0 >= d + dkv && pos == nullptr && ((pos_base + m0) & 3) == 0) {
             // V^T rows, consecutive positions: four tokens per thread along the row; a
             // quad that reaches past the last real row falls back to single stores
             const int nt = mcols >> 2;
@@ -369,7 +375,7 @@ struct EpiQKV {
                 const int tq = idx % nt, nl = idx / nt;
                 const int m = m0 + 4 * tq;
                 if (m >= M) continue;
-                const int nn = n0 + nl - 2 * d;
+                const int nn = n0 + nl - d - dkv;
                 const int h = nn / Dh, rr = nn - h * Dh;
                 T* dst = Vt + ((size_t)h * Dh + rr) * Cs + pos_base + m;
                 const float* y = Y + nl * ldy + 4 * tq;
@@ -390,7 +396,8 @@ struct EpiQKV {
             const int n = n0 + 2 * p;
             const float a = Y[(2 * p) * ldy + ml], b = Y[(2 * p + 1) * ldy + ml];
             const int ps = pos ? pos[m] : pos_base + m;
-            const int seg = n / d, nn = n - seg * d;
+            const int seg = n < d ? 0 : (n < d + dkv ? 1 : 2);
+            const int nn = n - (seg == 0 ? 0 : (seg == 1 ? d : d + dkv));
             const int h = nn / Dh, rr = nn - h * Dh;
             if (seg < 2) {
                 const int j = rr >> 1;

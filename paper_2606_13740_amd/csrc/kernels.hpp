@@ -310,18 +310,31 @@ struct PackSrc {
     int kind;
     int N;        // real packed rows
     int K;        // real columns
-    int d, Dh;    // for MAP_QKV
+    int d, Dh;    // for MAP_QKV: Q rows (H * Dh) and head size
+    int dkv;      // for MAP_QKV: K and V rows each (Hkv * Dh)
 };
 
+// MAP_QKV packed rows: [Q: d rows | K: dkv rows | V: dkv rows]; inside every Q or K
+// head, packed row 2i is dim i and 2i+1 is dim i + Dh/2 (a RoPE pair is adjacent).
 __device__ __forceinline__ const void* src_row(const PackSrc& p, int r, int& row) {
     if (r >= p.N) return nullptr;
     if (p.kind == MAP_IDENT) { row = r; return p.src[0]; }
     if (p.kind == MAP_GATEUP) { row = r >> 1; return p.src[r & 1]; }
-    const int seg = r / p.d, rr = r - seg * p.d;
+    const int seg = r < p.d ? 0 : (r < p.d + p.dkv ? 1 : 2);
+    const int rr = r - (seg == 0 ? 0 : (seg == 1 ? p.d : p.d + p.dkv));
     if (seg == 2) { row = rr; return p.src[2]; }
     const int h = rr / p.Dh, w = rr - h * p.Dh;
     row = h * p.Dh + (w >> 1) + (w & 1) * (p.Dh >> 1);   // adjacent packed rows = RoPE pair
     return p.src[seg];
+}
+
+// Q/K/V biases (fp32 vectors in p.src[0..2]) in packed-row order; padding rows 0.
+__global__ void __launch_bounds__(256) pack_bias_kernel(PackSrc p, int n_rows_padded, float* out) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n_rows_padded) return;
+    int row = 0;
+    const float* src = (const float*)src_row(p, r, row);
+    out[r] = src ? src[row] : 0.f;
 }
 
 // One thread per 16-byte lane slot.  ST: source element type (float / uint16_t bf16).

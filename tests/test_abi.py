@@ -60,6 +60,10 @@ def _create(dl, cfg):
     ("dtype", 7, -3),
     ("eps", 0.0, -1),
     ("block", 0, -1),
+    ("n_kv_heads", 3, -1),         # does not divide 4 query heads
+    ("n_kv_heads", 8, -1),         # more K/V heads than query heads
+    ("n_kv_heads", -1, -1),
+    ("qkv_bias", 2, -1),
 ])
 def test_model_create_validates_config(dl, field, value, code):
     cfg = dl.make_config(synth.TINY, "f32")
