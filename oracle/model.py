@@ -157,6 +157,49 @@ def dequantize_rows(q: np.ndarray, s: np.ndarray) -> np.ndarray:
 
 
 # -----------------------------------------------------------------------------
+# Q4_0 weights (Implementation section: the operator library's Q4_0 matrix
+# multiplication; Evaluation: all models run Q4_0).  The GGUF Q4_0 format: each
+# row is cut into blocks of 32 consecutive input columns; a block stores one fp16
+# scale d and 32 four-bit codes q in [0, 15]; a weight is (q - 8) * d.
+# -----------------------------------------------------------------------------
+
+Q4_BLOCK = 32
+
+
+def quantize_rows_q4_0(w: np.ndarray):
+    """Q4_0 quantisation of every row of w [N, K], decided in float32.
+
+    Per block: m = the block's value of largest magnitude (the first one in column
+    order on ties), keeping its sign; d = m / -8; id = 1 / d (0 if d = 0);
+    q = min(15, trunc(x * id + 8.5)) for every x of the block; the stored scale is
+    d rounded to fp16 (round to nearest even).  A ragged last block (K not a
+    multiple of 32) is padded with zeros.  Returns (q uint8 [N, nb*32], d float16
+    [N, nb]), nb = ceil(K / 32)."""
+    w = np.asarray(w, dtype=np.float32)
+    N, K = w.shape
+    nb = -(-K // Q4_BLOCK)
+    x = np.zeros((N, nb * Q4_BLOCK), np.float32)
+    x[:, :K] = w
+    x = x.reshape(N, nb, Q4_BLOCK)
+    first_max = np.argmax(np.abs(x), axis=2)                       # first index of max |x|
+    m = np.take_along_axis(x, first_max[:, :, None], axis=2)[:, :, 0]
+    d = (m / np.float32(-8.0)).astype(np.float32)
+    with np.errstate(divide="ignore"):
+        inv = np.where(d != 0, np.float32(1.0) / np.where(d != 0, d, np.float32(1.0)), np.float32(0.0))
+    inv = inv.astype(np.float32)
+    v = (x * inv[:, :, None]).astype(np.float32) + np.float32(8.5)   # float32 product, then float32 sum
+    q = np.minimum(np.trunc(v.astype(np.float32)), 15).astype(np.uint8)
+    return q.reshape(N, nb * Q4_BLOCK), d.astype(np.float16)
+
+
+def dequantize_q4_0(q: np.ndarray, d: np.ndarray, K: int) -> np.ndarray:
+    """Weights (q - 8) * d in float64, the padding columns dropped."""
+    N, nb = d.shape
+    w = (q.reshape(N, nb, Q4_BLOCK).astype(np.float64) - 8.0) * d.astype(np.float64)[:, :, None]
+    return w.reshape(N, nb * Q4_BLOCK)[:, :K]
+
+
+# -----------------------------------------------------------------------------
 # Model parameters
 # -----------------------------------------------------------------------------
 
@@ -178,13 +221,16 @@ class OracleModel:
     bit patterns), or a callable ``layer -> per-layer dict`` plus the globals, so
     that very large models can be materialised one layer at a time.
     With ``int8=True`` every matrix except the embedding is replaced by its
-    dequantised int8 form q * s (per output row).
+    dequantised int8 form q * s (per output row); with ``q4=True`` by its
+    dequantised Q4_0 form (q - 8) * d (per row and 32-column block).
     """
 
     def __init__(self, shape, weights: dict, int8: bool = False, cache_layers: Optional[bool] = None,
-                 layer_source=None):
+                 layer_source=None, q4: bool = False):
+        assert not (int8 and q4)
         self.shape = shape
         self.int8 = int8
+        self.q4 = q4
         self._src = weights
         self._layer_source = layer_source
         if cache_layers is None:
@@ -194,12 +240,15 @@ class OracleModel:
         self.final_norm = _f64(weights["final_norm"])
         self._lm_src = weights["lm_head"]
         self._lm = None
-        if self._cache is not None or int8:
+        if self._cache is not None or int8 or q4:
             self._lm = self._convert_matrix(self._lm_src)
 
     def _convert_matrix(self, w):
-        if self.int8:
+        if self.int8 or self.q4:
             wf = w if w.dtype == np.float32 else (w.astype(np.uint32) << 16).view(np.float32)
+            if self.q4:
+                q, d = quantize_rows_q4_0(wf)
+                return dequantize_q4_0(q, d, wf.shape[1])
             q, s = quantize_rows_int8(wf)
             return dequantize_rows(q, s)
         return _f64(w)

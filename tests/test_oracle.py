@@ -509,6 +509,84 @@ def test_int8_model_is_bf16_model_with_dequantised_weights():
     np.testing.assert_array_equal(m8.out, mref.out)
 
 
+# ----------------------------------------------------------------------------
+# Q4_0 weights
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_q4_0_recovers_representable_blocks_exactly(sign):
+    """A block whose values are (c - 8) * d0 with a power-of-two d0 and at least one
+    code 0 (the value -8 * d0 has the largest magnitude) quantises to exactly c and
+    d0; with the block negated, d = -d0 and the codes are the same."""
+    rng = np.random.default_rng(5)
+    N, nb = 6, 5
+    d0 = np.float32(2.0 ** -7)
+    c = rng.integers(0, 16, (N, nb * 32))
+    c[:, ::32] = 0                                     # a code 0 in every block
+    x = ((c - 8) * d0 * sign).astype(np.float32)
+    q, d = oracle.quantize_rows_q4_0(x)
+    np.testing.assert_array_equal(q, c)
+    np.testing.assert_array_equal(d.astype(np.float32), np.full((N, nb), d0 * sign, np.float32))
+    np.testing.assert_array_equal(oracle.dequantize_q4_0(q, d, nb * 32), x.astype(np.float64))
+
+
+def test_q4_0_error_bound_and_extreme_code():
+    """|w - (q - 8) d| <= |d| / 2 (+ the fp16 rounding of d), except where the code
+    clamps at 15 (w / d > 7.5), where it is <= |d|; the value of largest magnitude
+    of every block gets code 0.  Ragged K pads the last block with zeros."""
+    rng = np.random.default_rng(6)
+    K = 32 * 7 + 13
+    w = (rng.standard_normal((40, K)) * 0.02).astype(np.float32)
+    w[3, 32:64] = 0.0                                  # an all-zero block: d = 0, codes 8
+    q, d = oracle.quantize_rows_q4_0(w)
+    deq = oracle.dequantize_q4_0(q, d, K)
+    nb = d.shape[1]
+    xp = np.zeros((40, nb * 32), np.float64)
+    xp[:, :K] = w
+    dd = np.repeat(d.astype(np.float64), 32, axis=1)
+    d32 = np.repeat((np.max(np.abs(xp.reshape(40, nb, 32)), axis=2) / 8.0), 32, axis=1)   # |d| before fp16
+    ratio = np.divide(xp, np.sign(dd) * d32, out=np.zeros_like(xp), where=d32 > 0)         # w / d
+    bound = np.where(ratio > 7.5, 1.0, 0.5) * np.abs(dd) + 8.0 * np.abs(np.abs(dd) - d32) + 1e-12
+    err = np.abs(xp - np.pad(deq, ((0, 0), (0, nb * 32 - K))))
+    assert np.all(err <= bound)
+    first = np.argmax(np.abs(xp.reshape(40, nb, 32)), axis=2)
+    codes = q.reshape(40, nb, 32)
+    nz = np.abs(d.astype(np.float64)) > 0
+    assert np.all(np.take_along_axis(codes, first[:, :, None], axis=2)[:, :, 0][nz] == 0)
+    assert np.all(q.reshape(40, nb, 32)[3, 1] == 8) and d[3, 1] == 0
+
+
+def test_q4_0_sign_tie_goes_to_the_first_column():
+    x = np.zeros((1, 32), np.float32)
+    x[0, 4], x[0, 9] = 0.5, -0.5
+    q, d = oracle.quantize_rows_q4_0(x)
+    assert float(d[0, 0]) == -0.0625                   # m = +0.5 (column 4), d = m / -8
+    assert q[0, 4] == 0 and q[0, 9] == 15 and q[0, 0] == 8
+    np.testing.assert_array_equal(oracle.dequantize_q4_0(q, d, 32)[0, [4, 9]], [0.5, -0.4375])
+
+
+def test_q4_0_model_is_bf16_model_with_dequantised_weights():
+    sh = MICRO
+    w = synth.all_weights(sh, "bf16", 0)
+    m4 = oracle.OracleModel(sh, w, q4=True)
+    deq = lambda a: oracle.dequantize_q4_0(*oracle.quantize_rows_q4_0(synth.as_f32(a)), a.shape[1])
+    wd = dict(w)
+    wd["lm_head"] = deq(w["lm_head"])
+    wd["layers"] = []
+    for lw in w["layers"]:
+        dct = dict(lw)
+        for k in om.GEMM_WEIGHTS:
+            dct[k] = deq(lw[k])
+        wd["layers"].append(dct)
+    mref = oracle.OracleModel(sh, wd)
+    for m in (m4, mref):
+        kv = oracle.OracleKV(sh, 40)
+        oracle.prefill(m, kv, synth.prompt_ids(sh, 8))
+        m.out = oracle.denoise_step(m, kv, *synth.window(sh, 32, range(32))).logits
+    np.testing.assert_array_equal(m4.out, mref.out)
+
+
 def test_synth_inputs_are_reproducible_and_sliceable():
     a = synth.normal(0, 5, 1000, "bf16")
     b = synth.normal(0, 5, 101, "bf16", offset=333)
