@@ -34,6 +34,9 @@ WORKLOADS = {
                                         masked=list(range(24, 64)), segs=[(0, 32, 4), (32, 32, 4)], sls=True),
     "llada8b_w8_p4096_w64_spec": dict(shape="llada8b", dtype="w8", prefix=4096, W=64,
                                       masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)], sls=True),
+    # Q4_0 weights (the paper's own quantisation), otherwise config 2
+    "llada8b_q4_p512_w32": dict(shape="llada8b", dtype="q4", prefix=512, W=32,
+                                masked=list(range(8, 32)), segs=[(0, 32, 1)]),
     # Dream-7B (grouped-query attention, 28 query heads over 4 K/V heads, Q/K/V biases)
     "dream7b_bf16_p512_w32": dict(shape="dream7b", dtype="bf16", prefix=512, W=32,
                                   masked=list(range(8, 32)), segs=[(0, 32, 1)]),
@@ -415,7 +418,7 @@ def cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob, min_s=10.0):
 
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     sh1 = shape.with_layers(1)
-    om = oracle.OracleModel(sh1, dict(glob, layers=None), int8=(dtype == "w8"), cache_layers=True,
+    om = oracle.OracleModel(sh1, dict(glob, layers=None), int8=(dtype == "w8"), q4=(dtype == "q4"), cache_layers=True,
                             layer_source=lambda l: synth.layer_weights(shape, l, "bf16"))
     kv = oracle.OracleKV(sh1, wl["prefix"] + wl["W"])
     oracle.prefill(om, kv, prompt)        # setup, not timed
@@ -574,7 +577,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if dtype == "bf16" else "int8w-bf16a",
+        "dtype": {"bf16": "bf16", "w8": "int8w-bf16a", "q4": "q4_0w-bf16a"}[dtype],
         "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
         "config": {"workload": args.workload, "layers": shape.n_layers, "d_model": shape.d_model,
                    "heads": shape.n_heads, "kv_heads": shape.kv_heads, "head_dim": shape.head_dim,

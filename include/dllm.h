@@ -66,6 +66,7 @@ extern "C" {
 #define DLLM_F32 0   /* fp32 weights, fp32 activations and KV cache */
 #define DLLM_BF16 1  /* bf16 weights; activations, Q and the KV cache as bf16 hi/lo pairs; fp32 accumulate */
 #define DLLM_W8 2    /* int8 weights with fp32 per-output-row scales; activations as for DLLM_BF16 */
+#define DLLM_Q4 3    /* Q4_0 weights (see dllm_quantize_q4_0); activations as for DLLM_BF16 */
 
 typedef struct dllm_model dllm_model;
 typedef struct dllm_kv dllm_kv;
@@ -82,7 +83,7 @@ typedef struct dllm_config {
     int32_t block;       /* block size of the block-causal prefix (32) */
     float eps;           /* RMSNorm epsilon */
     float rope_base;     /* RoPE base (10000) */
-    int32_t dtype;       /* DLLM_F32, DLLM_BF16 or DLLM_W8 */
+    int32_t dtype;       /* DLLM_F32, DLLM_BF16, DLLM_W8 or DLLM_Q4 */
     int32_t max_window;  /* largest row count of a step / append / refresh call (<= 256) */
     int32_t max_pos;     /* positions covered by the RoPE table; bounds every KV capacity */
     int32_t n_kv_heads;  /* K/V heads (grouped-query attention); 0 = n_heads; must divide n_heads */
@@ -90,7 +91,8 @@ typedef struct dllm_config {
 } dllm_config;
 
 /* Device pointers to row-major [out][in] matrices of one layer.
- * DLLM_F32: float; DLLM_BF16 and DLLM_W8: bfloat16 (W8 quantises them on create).
+ * DLLM_F32: float; DLLM_BF16, DLLM_W8 and DLLM_Q4: bfloat16 (W8 and Q4 quantise them
+ * on create).
  * wq, wo: [d][d]; wk, wv: [dkv][d] with dkv = n_kv_heads * head_dim; wg, wu:
  * [d_ff][d]; wd: [d][d_ff]; norms: float [d]; biases (read only when
  * cfg.qkv_bias, else may be NULL): float bq [d], bk [dkv], bv [dkv]. */
@@ -125,7 +127,9 @@ const char* dllm_version(void);
 /* Creates a model: validates the config, allocates the library's own copy of the
  * weights prepacked into MFMA-fragment order (and, for DLLM_W8, quantises every
  * matrix except the embedding to int8 with per-output-row fp32 scales
- * s = max|w| / 127, q = round-half-even(w / s), decided in fp32), builds the
+ * s = max|w| / 127, q = round-half-even(w / s), decided in fp32; for DLLM_Q4, to
+ * Q4_0 as dllm_quantize_q4_0 does, and the matrix products then use the weights
+ * (q - 8) * d exactly, with no rounding of the dequantised values), builds the
  * RoPE table, and allocates workspaces for max_window rows.  The caller's weight
  * buffers are only read during this call (on `stream`, which is synchronised
  * before returning) and may be freed afterwards.  Quantisation is the analog of
@@ -343,6 +347,22 @@ int dllm_accept_drafts(const float* d_conf, const int32_t* d_id, const int32_t* 
  * where d_mask[i] = 1, else -1, for n position-aligned entries (n >= 1). */
 int dllm_record_drafts(const int32_t* d_id, const uint8_t* d_mask, int32_t* d_draft_id, int32_t n,
                        dllm_stream stream);
+
+/* Q4_0 quantisation, the converter step for DLLM_Q4 models (Implementation: the
+ * operator library has a Q4_0 matrix multiplication and the model converter packs
+ * quantised weights; Evaluation: every model runs Q4_0).  The GGUF Q4_0 format:
+ * each row of the row-major [rows][K] source (float for src_dtype DLLM_F32,
+ * bfloat16 for DLLM_BF16; device) is cut into nb = ceil(K / 32) blocks of 32
+ * columns, a ragged last block padded with zeros.  Per block, in fp32: m = the
+ * value of largest magnitude (the first in column order on ties) with its sign,
+ * d = m / -8, inv = 1 / d (0 if d = 0), and every value x gets the code
+ * q = min(15, trunc(x * inv + 8.5)); the weight it stands for is (q - 8) * d16
+ * with d16 = d rounded to fp16 (nearest even).  Writes d_codes [rows][nb * 32]
+ * (one code per byte, padding columns included) and d_scales [rows][nb] (fp16
+ * bit patterns), both caller-owned device buffers, asynchronously on `stream`.
+ * E_INVAL for NULL pointers or rows, K < 1; E_DTYPE for another src_dtype. */
+int dllm_quantize_q4_0(const void* d_src, int32_t src_dtype, int32_t rows, int32_t K, uint8_t* d_codes,
+                       uint16_t* d_scales, dllm_stream stream);
 
 /* Measurement helper: one launch of a plain streaming read over `bytes` bytes of
  * the device buffer d_buf (16-byte aligned; bytes a multiple of 16), the same

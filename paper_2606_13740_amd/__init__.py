@@ -15,7 +15,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdllm.so")
 
 DLLM_OK, DLLM_E_INVAL, DLLM_E_CAPACITY, DLLM_E_DTYPE, DLLM_E_HIP, DLLM_E_UNIMPL, DLLM_E_NOMEM = 0, -1, -2, -3, -4, -5, -6
-DLLM_F32, DLLM_BF16, DLLM_W8 = 0, 1, 2
+DLLM_F32, DLLM_BF16, DLLM_W8, DLLM_Q4 = 0, 1, 2, 3
 K_QKV, K_ATTN, K_OPROJ, K_GATEUP, K_DOWN, K_LMHEAD = range(6)
 KERNEL_CLASSES = {"qkv": K_QKV, "attn": K_ATTN, "oproj": K_OPROJ, "gateup": K_GATEUP, "down": K_DOWN,
                   "lmhead": K_LMHEAD}
@@ -76,6 +76,7 @@ _SIGNATURES = {
     "dllm_probe_read": ([_vp, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dllm_kernel_bytes": ([_vp, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dllm_read_bandwidth": ([_vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
+    "dllm_quantize_q4_0": ([_vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_commit_staged": ([_vp, _vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_float, ctypes.c_float, _vp, _vp, _vp],
                            ctypes.c_int),
 }
@@ -247,6 +248,11 @@ def dllm_commit_staged(conf, ids, tok, mask, state, seg_begin: int, seg_len: int
                                     _stream(stream)), "dllm_commit_staged")
 
 
+def dllm_quantize_q4_0(src, src_dtype: int, rows: int, K: int, codes, scales, stream=None):
+    _check(lib().dllm_quantize_q4_0(_ptr(src), src_dtype, rows, K, _ptr(codes), _ptr(scales), _stream(stream)),
+           "dllm_quantize_q4_0")
+
+
 def dllm_read_bandwidth(buf, nbytes: int, sink, stream=None):
     _check(lib().dllm_read_bandwidth(_ptr(buf), nbytes, _ptr(sink), _stream(stream)), "dllm_read_bandwidth")
 
@@ -256,7 +262,7 @@ def dllm_read_bandwidth(buf, nbytes: int, sink, stream=None):
 # ----------------------------------------------------------------------------
 
 
-DTYPES = {"f32": DLLM_F32, "bf16": DLLM_BF16, "w8": DLLM_W8}
+DTYPES = {"f32": DLLM_F32, "bf16": DLLM_BF16, "w8": DLLM_W8, "q4": DLLM_Q4}
 
 
 def make_config(shape, dtype: str, max_window: int = 64, max_pos: int = 8192) -> dllm_config:

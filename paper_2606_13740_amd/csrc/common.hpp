@@ -12,7 +12,7 @@ typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 namespace dllm {
 
 // Weight element types of the packed GEMM operand.
-enum WType : int { WT_F32 = 0, WT_BF16 = 1, WT_I8 = 2 };
+enum WType : int { WT_F32 = 0, WT_BF16 = 1, WT_I8 = 2, WT_Q4 = 3 };
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
@@ -42,7 +42,13 @@ template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { re
 //   bf16 (KC = 32): lane l bytes = row l%16, cols 8g .. 8g+7
 //   f32  (KC = 16): lane l float s = row l%16, col 4s + g (s = 0..3, one MFMA each)
 //   int8 (KC = 64): lane l byte 8h + e = row l%16, col 32h + 8g + e (h = 0..1)
-// Packed weights: chunk (nt, kc) at byte ((nt * KCn + kc) * 64 + lane) * 16.
+//   Q4_0 (KC = 64, 512-byte chunks, 8 bytes per lane): dword h (= 32-column block
+//        h) of lane l holds the 4-bit codes of row l%16, cols 32h + 8g + e, e = 0..7,
+//        code e at bits 4 * (e / 2) (e even) or 16 + 4 * (e / 2) (e odd), so that
+//        one shift-and-mask yields two bf16 values of adjacent columns (q4_unpack);
+//        the chunk's fp16 scales sit in a separate array, 16 rows x 2 blocks.
+// Packed weights: chunk (nt, kc) at byte ((nt * KCn + kc) * 64 + lane) * 16
+// (Q4_0: * 8).
 //
 // Activation fragments use the same chunk shape with rows = tokens.  For fp32
 // models a chunk holds 16 fp32 columns.  For bf16 / int8-weight models a value v
@@ -57,6 +63,10 @@ template <int WT> struct WTraits;
 template <> struct WTraits<WT_F32> { static constexpr int KC = 16; static constexpr int XPER = 1; };
 template <> struct WTraits<WT_BF16> { static constexpr int KC = 32; static constexpr int XPER = 1; };
 template <> struct WTraits<WT_I8> { static constexpr int KC = 64; static constexpr int XPER = 2; };
+template <> struct WTraits<WT_Q4> { static constexpr int KC = 64; static constexpr int XPER = 2; };
+
+// Bytes of one packed weight chunk (16 rows x KC columns).
+template <int WT> constexpr int wchunk_bytes() { return WT == WT_Q4 ? 512 : 1024; }
 
 // Bytes of one activation chunk.
 template <bool F32> struct XChunk { static constexpr int bytes = F32 ? 1024 : 2048; };
@@ -137,6 +147,47 @@ __device__ __forceinline__ u32x4_t i8x8_to_bf16x8(uint32_t lo, uint32_t hi) {
     return r;
 }
 
+// Q4_0: four dwords of bf16 pairs (128 + q) for the 8 codes of one dword (see the
+// chunk layout above); 128 + q is exact in bf16 (7 stored significand bits).
+__device__ __forceinline__ u32x4_t q4_unpack(uint32_t c) {
+    u32x4_t r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = ((c >> (4 * i)) & 0x000F000Fu) | 0x43004300u;
+    return r;
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+__device__ __forceinline__ uint16_t f32_to_f16_bits(float f) {
+    return __builtin_bit_cast(uint16_t, (_Float16)f);    // round to nearest even
+}
+
+// Q4_0 decision for one block of 32 columns [k0, k0 + 32) of a row (columns >= K
+// read as 0), in fp32: m = the value of largest magnitude (first in column order),
+// d = m / -8, inv = 1 / d (0 when d = 0).  A value x gets code min(15, trunc(x * inv + 8.5)).
+template <typename ST>
+__device__ __forceinline__ void q4_block(const ST* row, int k0, int K, float& d, float& inv) {
+    float amax = 0.f, m = 0.f;
+    for (int k = k0; k < k0 + 32; ++k) {
+        const float x = (k < K) ? to_f32<ST>(row[k]) : 0.f;
+        if (fabsf(x) > amax) { amax = fabsf(x); m = x; }
+    }
+    d = __fdiv_rn(m, -8.0f);
+    inv = (d != 0.f) ? __fdiv_rn(1.0f, d) : 0.f;
+}
+
+// The product and the sum are rounded separately (no fused multiply-add), as the
+// format's reference arithmetic does: a fused x * inv + 8.5 moves codes that sit on a
+// rounding boundary.
+__device__ __forceinline__ uint32_t q4_code(float x, float inv) {
+#pragma clang fp contract(off)
+    const float p = x * inv;
+    const int q = (int)(p + 8.5f);
+    return (uint32_t)min(15, q);
+}
+
 __device__ __forceinline__ float warp_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -151,6 +202,9 @@ __device__ __forceinline__ float warp_max(float v) {
 __device__ __forceinline__ u32x4_t ldg16(const void* p) { return *(const u32x4_t*)p; }
 __device__ __forceinline__ u32x4_t ldg16_nt(const void* p) {
     return __builtin_nontemporal_load((const u32x4_t*)p);
+}
+__device__ __forceinline__ u32x2_t ldg8_nt(const void* p) {
+    return __builtin_nontemporal_load((const u32x2_t*)p);
 }
 
 }  // namespace dllm

@@ -46,6 +46,8 @@ inline long round_up(long a, long b) { return (a + b - 1) / b * b; }
 struct PackedW {
     void* w = nullptr;      // chunks
     float* scale = nullptr; // per packed row (int8) or nullptr
+    uint16_t* qs = nullptr; // Q4_0 block scales (fp16) or nullptr
+    size_t qs_bytes = 0;
     int N = 0;              // real rows
     int K = 0;              // real columns
     int n_tiles = 0;
@@ -102,6 +104,7 @@ struct dllm_model {
     float2* rope = nullptr;
     void* wpool = nullptr;   // packed weights of every matrix
     float* spool = nullptr;  // int8 scales
+    uint16_t* qpool = nullptr;  // Q4_0 scales
     float* gpool = nullptr;  // norm gains
     float* bpool = nullptr;  // Q/K/V biases
     Workspace ws;
@@ -160,13 +163,17 @@ struct Decomp {
 
 constexpr int N_CU = 256;
 
-int template_fw(GemmKind k) { return k == G_QKV ? 3 : (k == G_GU ? 6 : (k == G_LM ? 8 : 4)); }
+// Q4_0 gate/up keeps 4 tiles: at 6 its two-stage pipeline of codes, scales and hi/lo
+// activations does not fit 256 VGPRs.
+constexpr int template_fw(GemmKind k, int wt) {
+    return k == G_QKV ? 3 : (k == G_GU ? (wt == WT_Q4 ? 4 : 6) : (k == G_LM ? 8 : 4));
+}
 int template_nwn(GemmKind k) { return k == G_LM ? 4 : 1; }
 
-Decomp decomp(GemmKind k, int n_tiles, int Mc, int gy) {
+Decomp decomp(GemmKind k, int wt, int n_tiles, int Mc, int gy) {
     const int min_tiles = (k == G_QKV || k == G_RES) ? 128 : (k == G_GU ? 256 : 512);
     if (n_tiles < min_tiles) return Decomp{true, 1, 1};
-    const int fw = template_fw(k), nwn = template_nwn(k);
+    const int fw = template_fw(k, wt), nwn = template_nwn(k);
     Decomp best{false, 1, 1};
     double best_load = 1e30;
     for (int tpg = fw; tpg >= 1; --tpg) {
@@ -207,7 +214,7 @@ int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const
     g.tpg = dc.tpg;
     if (dc.small) return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, dc.ks, gy, s);
     if constexpr (KIND == G_QKV) return launch_gemm_mt<WT, 3, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
-    else if constexpr (KIND == G_GU) return launch_gemm_mt<WT, 6, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
+    else if constexpr (KIND == G_GU) return launch_gemm_mt<WT, template_fw(G_GU, WT), 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
     else if constexpr (KIND == G_LM) return launch_gemm_mt<WT, 8, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
     else return launch_gemm_mt<WT, 4, 1, 8>(MT, g, epi, n_tiles, dc.ks, gy, s);
 }
@@ -300,14 +307,18 @@ void plan_packed(PackedW& p, int wt, int N, int K) {
     p.K = K;
     p.n_tiles = ceil_div(N, 16);
     p.KCw = ceil_div(K, kc_of(wt));
-    p.bytes = (size_t)p.n_tiles * p.KCw * 1024;
+    p.bytes = (size_t)p.n_tiles * p.KCw * (wt == WT_Q4 ? 512 : 1024);
+    p.qs_bytes = (wt == WT_Q4) ? (size_t)p.n_tiles * p.KCw * 64 : 0;   // 16 rows x 2 blocks x fp16
 }
 
 template <typename ST>
 int pack_one(dllm_model* m, PackedW& p, const PackSrc& src, hipStream_t s) {
     const size_t units = (size_t)p.n_tiles * p.KCw * 64;
     const int blocks = ceil_div((long)units, 256);
-    if (m->wt == WT_I8) {
+    if (m->wt == WT_Q4) {
+        hipLaunchKernelGGL((pack_q4_kernel<ST>), dim3(blocks), dim3(256), 0, s, src, p.n_tiles, p.KCw, (u32x2_t*)p.w,
+                           p.qs);
+    } else if (m->wt == WT_I8) {
         hipLaunchKernelGGL((row_scale_kernel<ST>), dim3(p.n_tiles * 16), dim3(256), 0, s, src, p.n_tiles * 16, p.scale);
         hipLaunchKernelGGL((pack_kernel<WT_I8, ST>), dim3(blocks), dim3(256), 0, s, src, p.n_tiles, p.KCw,
                            (u32x4_t*)p.w, (const float*)p.scale);
@@ -332,13 +343,13 @@ int validate_config(const dllm_config* c) {
     if (c->max_window < 1 || c->max_window > 256) return fail(DLLM_E_INVAL, "max_window must be in [1, 256]");
     if (c->max_pos < 1) return fail(DLLM_E_INVAL, "max_pos must be >= 1");
     if (!(c->eps > 0.f) || !(c->rope_base > 1.f)) return fail(DLLM_E_INVAL, "eps must be > 0 and rope_base > 1");
-    if (c->dtype != DLLM_F32 && c->dtype != DLLM_BF16 && c->dtype != DLLM_W8)
-        return fail(DLLM_E_DTYPE, "dtype must be DLLM_F32, DLLM_BF16 or DLLM_W8");
+    if (c->dtype != DLLM_F32 && c->dtype != DLLM_BF16 && c->dtype != DLLM_W8 && c->dtype != DLLM_Q4)
+        return fail(DLLM_E_DTYPE, "dtype must be DLLM_F32, DLLM_BF16, DLLM_W8 or DLLM_Q4");
     if (c->dtype == DLLM_F32) {
         if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
             return fail(DLLM_E_DTYPE, "fp32 models need head_dim 32, 64 or 128");
     } else if (c->head_dim != 64 && c->head_dim != 128) {
-        return fail(DLLM_E_DTYPE, "bf16 / int8 models need head_dim 64 or 128");
+        return fail(DLLM_E_DTYPE, "bf16 / int8 / Q4_0 models need head_dim 64 or 128");
     }
     if (c->d_model % 32 != 0) return fail(DLLM_E_DTYPE, "d_model must be a multiple of 32");
     if (c->d_model > 4 * ROW_NT * ROW_VPT) return fail(DLLM_E_DTYPE, "d_model must be <= 8192");
@@ -379,10 +390,11 @@ int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* g
                   hipStream_t s, bool sel = false, const uint8_t* need = nullptr, int n_sel = 0) {
     Workspace& w = m->ws;
     const int d = m->cfg.d_model;
-    const Decomp dc = decomp(G_RES, W.n_tiles, Mc, gy);
+    const Decomp dc = decomp(G_RES, WT, W.n_tiles, Mc, gy);
     const int KS = dc.ks;
     if ((size_t)KS * Mc * d > w.part_floats) return fail(DLLM_E_INVAL, "internal: split-K buffer too small");
     GemmArgs g{W.w, W.scale, X, W.KCw, W.KCw * WTraits<WT>::XPER, W.n_tiles};
+    g.qs = W.qs;
     EpiPartial e{w.part, d, Mc};
     int rc = launch_gemm<WT, G_RES>(dc, W.n_tiles, MT, g, e, gy, s);
     if (rc) return rc;
@@ -429,10 +441,11 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
         {
             GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles, L.bqkv};
+            g.qs = L.qkv.qs;
             EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane,
                            kv->Cs};
             ProbeScope ps(m, DLLM_K_QKV, s);
-            if ((rc = launch_gemm<WT, G_QKV>(decomp(G_QKV, L.qkv.n_tiles, Mc, gy), L.qkv.n_tiles, MT, g, e, gy, s)))
+            if ((rc = launch_gemm<WT, G_QKV>(decomp(G_QKV, WT, L.qkv.n_tiles, Mc, gy), L.qkv.n_tiles, MT, g, e, gy, s)))
                 return rc;
         }
         // attention over [0, T) (+ split merge)
@@ -482,9 +495,10 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         // RMSNorm + gate/up + SwiGLU
         {
             GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles};
+            g.qs = L.gu.qs;
             EpiSwiGLU<XF32> e{w.af, m->KCx_f};
             ProbeScope ps(m, DLLM_K_GATEUP, s);
-            if ((rc = launch_gemm<WT, G_GU>(decomp(G_GU, L.gu.n_tiles, Mc, gy), L.gu.n_tiles, MT, g, e, gy, s)))
+            if ((rc = launch_gemm<WT, G_GU>(decomp(G_GU, WT, L.gu.n_tiles, Mc, gy), L.gu.n_tiles, MT, g, e, gy, s)))
                 return rc;
         }
         // down projection + residual (+ next norm operand)
@@ -508,7 +522,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         }
         if (gyl * MTl * 16 > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
         GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles};
-        const Decomp dc = decomp(G_LM, m->lm.n_tiles, gyl * MTl * 16, gyl);
+        g.qs = m->lm.qs;
+        const Decomp dc = decomp(G_LM, WT, m->lm.n_tiles, gyl * MTl * 16, gyl);
         const int gx = row_groups(dc, m->lm.n_tiles);
         if (gx > m->n_lm_wg) return fail(DLLM_E_INVAL, "internal: LM-head partials exceed their buffer");
         if (Ml > 0) {
@@ -526,6 +541,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
 int forward(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     if (m->wt == WT_F32) return forward_t<WT_F32, float>(m, kv, a, s);
     if (m->wt == WT_BF16) return forward_t<WT_BF16, uint16_t>(m, kv, a, s);
+    if (m->wt == WT_Q4) return forward_t<WT_Q4, uint16_t>(m, kv, a, s);
     return forward_t<WT_I8, uint16_t>(m, kv, a, s);
 }
 
@@ -566,27 +582,32 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     dllm_model* m = new dllm_model();
     m->cfg = *cfg;
     const dllm_config& c = m->cfg;
-    m->wt = c.dtype == DLLM_F32 ? WT_F32 : (c.dtype == DLLM_BF16 ? WT_BF16 : WT_I8);
+    m->wt = c.dtype == DLLM_F32 ? WT_F32 : (c.dtype == DLLM_BF16 ? WT_BF16 : (c.dtype == DLLM_W8 ? WT_I8 : WT_Q4));
     m->xf32 = c.dtype == DLLM_F32;
     m->kv_elem = 4;
     m->Hkv = c.n_kv_heads > 0 ? c.n_kv_heads : c.n_heads;
     m->dkv = m->Hkv * c.head_dim;
     const int xcols = m->xf32 ? 16 : 32;
-    const int xper = m->wt == WT_I8 ? 2 : 1;
+    const int xper = (m->wt == WT_I8 || m->wt == WT_Q4) ? 2 : 1;
     const int d = c.d_model, F = c.d_ff;
 
     m->layers.resize(c.n_layers);
-    size_t wbytes = 0, srows = 0;
+    size_t wbytes = 0, srows = 0, qbytes = 0;
     for (auto& L : m->layers) {
         plan_packed(L.qkv, m->wt, d + 2 * m->dkv, d);
         plan_packed(L.o, m->wt, d, d);
         plan_packed(L.gu, m->wt, 2 * F, d);
         plan_packed(L.down, m->wt, d, F);
-        for (PackedW* p : {&L.qkv, &L.o, &L.gu, &L.down}) { wbytes += p->bytes; srows += p->n_tiles * 16; }
+        for (PackedW* p : {&L.qkv, &L.o, &L.gu, &L.down}) {
+            wbytes += p->bytes;
+            srows += p->n_tiles * 16;
+            qbytes += p->qs_bytes;
+        }
     }
     plan_packed(m->lm, m->wt, c.vocab, d);
     wbytes += m->lm.bytes;
     srows += m->lm.n_tiles * 16;
+    qbytes += m->lm.qs_bytes;
     m->KCx_d = m->layers[0].qkv.KCw * xper;
     m->KCx_f = m->layers[0].down.KCw * xper;
     (void)xcols;
@@ -598,6 +619,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     };
     if ((rc = alloc_zero(&m->wpool, wbytes))) return cleanup(rc);
     if (m->wt == WT_I8 && (rc = alloc_zero((void**)&m->spool, srows * 4))) return cleanup(rc);
+    if (m->wt == WT_Q4 && (rc = alloc_zero((void**)&m->qpool, qbytes))) return cleanup(rc);
     if ((rc = alloc_zero((void**)&m->gpool, (size_t)(2 * c.n_layers + 1) * d * 4))) return cleanup(rc);
     const int qkv_rows = m->layers[0].qkv.n_tiles * 16;     // packed (padded) Q/K/V rows
     if (c.qkv_bias && (rc = alloc_zero((void**)&m->bpool, (size_t)c.n_layers * qkv_rows * 4))) return cleanup(rc);
@@ -609,10 +631,12 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     // carve
     char* wp = (char*)m->wpool;
     float* sp = m->spool;
+    char* qp = (char*)m->qpool;
     auto carve = [&](PackedW& p) {
         p.w = wp;
         wp += p.bytes;
         if (sp) { p.scale = sp; sp += p.n_tiles * 16; }
+        if (qp) { p.qs = (uint16_t*)qp; qp += p.qs_bytes; }
     };
     for (auto& L : m->layers) { carve(L.qkv); carve(L.o); carve(L.gu); carve(L.down); }
     carve(m->lm);
@@ -663,7 +687,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
 int dllm_model_destroy(dllm_model* m) {
     if (!m) return DLLM_OK;
     free_ws(m->ws);
-    void* ptrs[] = {m->wpool, m->spool, m->gpool, m->bpool, m->embed, m->rope};
+    void* ptrs[] = {m->wpool, m->spool, m->qpool, m->gpool, m->bpool, m->embed, m->rope};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     for (auto e : m->ev_b) (void)hipEventDestroy(e);
@@ -948,7 +972,8 @@ int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms) {
 int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes) {
     if (!m || !bytes) return fail(DLLM_E_INVAL, "NULL argument");
     const dllm_config& c = m->cfg;
-    const double wsz = m->wt == WT_F32 ? 4.0 : (m->wt == WT_BF16 ? 2.0 : 1.0);
+    // bytes per weight (Q4_0: a 4-bit code plus a 2-byte scale per 32 weights)
+    const double wsz = m->wt == WT_F32 ? 4.0 : (m->wt == WT_BF16 ? 2.0 : (m->wt == WT_I8 ? 1.0 : 0.5 + 2.0 / 32));
     const double asz = (double)m->kv_elem;   // activations and cache values: 4 bytes
     const double d = c.d_model, F = c.d_ff, V = c.vocab, dkv = m->dkv;
     const double scale_b = (m->wt == WT_I8) ? 4.0 : 0.0;   // per weight row
@@ -1002,6 +1027,23 @@ int dllm_record_drafts(const int32_t* d_id, const uint8_t* d_mask, int32_t* d_dr
     if (n < 1) return fail(DLLM_E_INVAL, "n must be >= 1");
     hipLaunchKernelGGL(record_drafts_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, (hipStream_t)stream,
                        (const int*)d_id, d_mask, (int*)d_draft_id, n);
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
+int dllm_quantize_q4_0(const void* d_src, int32_t src_dtype, int32_t rows, int32_t K, uint8_t* d_codes,
+                       uint16_t* d_scales, dllm_stream stream) {
+    if (!d_src || !d_codes || !d_scales) return fail(DLLM_E_INVAL, "NULL argument");
+    if (rows < 1 || K < 1) return fail(DLLM_E_INVAL, "rows and K must be >= 1");
+    if (src_dtype != DLLM_F32 && src_dtype != DLLM_BF16) return fail(DLLM_E_DTYPE, "source must be DLLM_F32 or DLLM_BF16");
+    const long n = (long)rows * ceil_div(K, 32);
+    const int blocks = ceil_div(n, 256);
+    if (src_dtype == DLLM_F32)
+        hipLaunchKernelGGL((quantize_q4_kernel<float>), dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                           (const float*)d_src, rows, K, d_codes, d_scales);
+    else
+        hipLaunchKernelGGL((quantize_q4_kernel<uint16_t>), dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                           (const uint16_t*)d_src, rows, K, d_codes, d_scales);
     HIP_TRY(hipGetLastError());
     return DLLM_OK;
 }

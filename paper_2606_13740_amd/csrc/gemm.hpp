@@ -30,6 +30,7 @@ struct GemmArgs {
     int n_tiles;          // packed rows / 16
     const float* bias = nullptr;  // per packed row (added after the row scale) or nullptr
     int tpg = 0;          // row tiles per wave group (1 .. FW); the launch sets it
+    const uint16_t* qs = nullptr;  // Q4_0: fp16 scales [tile][chunk][16 rows][2 blocks]
 };
 
 // Epilogue interface:
@@ -50,6 +51,12 @@ struct GemmArgs {
 template <int WT, int F, int MT>
 constexpr int pipeline_depth() {
     constexpr int XP = (WT == WT_F32) ? 1 : 2;
+    if constexpr (WT == WT_Q4) {
+        // 8-byte code loads + a scale dword per tile, 16 activation dwords per token
+        // tile: two stages up to 2 token tiles, one beyond (the accumulators of 3-4
+        // token tiles leave no room for a second)
+        return MT <= 2 ? 2 : 1;
+    }
     constexpr int slot = 4 * (F + MT * WTraits<WT>::XPER * XP);
     constexpr int d = 128 / slot;
     return d < 1 ? 1 : (d > 8 ? 8 : d);
@@ -124,17 +131,30 @@ gemm_kernel(GemmArgs g, Epi epi) {
         const unsigned span = (unsigned)(kb1 - kb0);
         const int c0 = kb0 + (int)(((unsigned)wk * span) / NWk);
         const int c1 = kb0 + (int)(((unsigned)(wk + 1) * span) / NWk);
-        const char* wp = (const char*)g.W + ((size_t)nt0 * g.KCw * 64 + lane) * 16;
+        constexpr int WCB = wchunk_bytes<WT>();
+        const char* wp = (const char*)g.W + ((size_t)nt0 * g.KCw * 64 + lane) * (WCB / 64);
         const char* xp = (const char*)g.X + (size_t)mt0 * g.KCx * XB + lane * 16;
-        const size_t wtile = (size_t)g.KCw * 1024, xtile = (size_t)g.KCx * XB;
+        const size_t wtile = (size_t)g.KCw * WCB, xtile = (size_t)g.KCx * XB;
+        // Q4_0 scales of this lane's row: one dword (two fp16) per chunk
+        [[maybe_unused]] const uint32_t* qsp =
+            (WT == WT_Q4) ? (const uint32_t*)g.qs + (size_t)nt0 * g.KCw * 16 + (lane & 15) : nullptr;
 
-        u32x4_t wb[D][FW];
+        u32x4_t wb[D][FW];                    // weight chunks (bf16 / int8 / fp32)
+        [[maybe_unused]] u32x2_t wq[D][FW];   // Q4_0 codes
+        [[maybe_unused]] uint32_t wsc[D][FW]; // Q4_0 scales (two fp16)
         u32x4_t xb[D][MT * XPER * XP];
 
         auto load = [&](int s, int c) {
 #pragma unroll
-            for (int f = 0; f < FW; ++f)
-                if (f < nf) wb[s][f] = ldg16_nt(wp + f * wtile + (size_t)c * 1024);
+            for (int f = 0; f < FW; ++f) {
+                if (f >= nf) continue;
+                if constexpr (WT == WT_Q4) {
+                    wq[s][f] = ldg8_nt(wp + f * wtile + (size_t)c * WCB);
+                    wsc[s][f] = qsp[((size_t)f * g.KCw + c) * 16];
+                } else {
+                    wb[s][f] = ldg16_nt(wp + f * wtile + (size_t)c * WCB);
+                }
+            }
 #pragma unroll
             for (int t = 0; t < MT; ++t)
 #pragma unroll
@@ -145,6 +165,38 @@ gemm_kernel(GemmArgs g, Epi epi) {
                             ldg16(xp + t * xtile + (size_t)(c * XPER + h) * XB + pl * 1024);
         };
         auto compute = [&](int s) {
+            // Q4_0 (weights as the B operand, so a lane's accumulator column is one
+            // weight row and takes one scale per block): codes unpack to bf16 128 + q,
+            // so a block's MFMAs start from zp = -136 * sum_k x and give
+            // sum_k (q - 8) x exactly up to fp32 accumulation; then acc += d * that.
+            if constexpr (WT == WT_Q4) {
+                const u32x4_t ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    f32x4_t zp[MT];
+#pragma unroll
+                    for (int t = 0; t < MT; ++t) {
+                        f32x4_t z = mfma_bf16(xb[s][(t * 2 + h) * 2 + 0], ones, f32x4_t{0.f, 0.f, 0.f, 0.f});
+                        z = mfma_bf16(xb[s][(t * 2 + h) * 2 + 1], ones, z);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) zp[t][i] = -136.0f * z[i];
+                    }
+#pragma unroll
+                    for (int f = 0; f < FW; ++f) {
+                        if (f >= nf) continue;
+                        const float sc = f16_bits_to_f32(h == 0 ? (wsc[s][f] & 0xFFFFu) : (wsc[s][f] >> 16));
+                        const u32x4_t w = q4_unpack(wq[s][f][h]);
+#pragma unroll
+                        for (int t = 0; t < MT; ++t) {
+                            f32x4_t v = mfma_bf16(xb[s][(t * 2 + h) * 2 + 0], w, zp[t]);
+                            v = mfma_bf16(xb[s][(t * 2 + h) * 2 + 1], w, v);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) acc[f][t][i] = fmaf(sc, v[i], acc[f][t][i]);
+                        }
+                    }
+                }
+                return;
+            }
 #pragma unroll
             for (int f = 0; f < FW; ++f) {
                 if (f >= nf) continue;
@@ -207,7 +259,9 @@ gemm_kernel(GemmArgs g, Epi epi) {
                 for (int t = 0; t < MT; ++t)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        float* p = slot + (16 * f + 4 * gq + i) * LDY + 16 * t + r;
+                        // Q4_0 accumulators are transposed: element i is token 4gq + i of row r
+                        float* p = (WT == WT_Q4) ? slot + (16 * f + r) * LDY + 16 * t + 4 * gq + i
+                                                 : slot + (16 * f + 4 * gq + i) * LDY + 16 * t + r;
                         *p = (k0 == 0) ? acc[f][t][i] : *p + acc[f][t][i];
                     }
         }

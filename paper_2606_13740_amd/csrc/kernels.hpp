@@ -392,6 +392,68 @@ pack_kernel(PackSrc p, int n_tiles, int KCw, u32x4_t* out, const float* scale) {
     out[u] = v;
 }
 
+// Q4_0 prepack: one thread per lane slot of a 512-byte chunk (16 rows x 64
+// columns = two 32-column blocks): the lane's 8 codes of each block in the dword
+// order q4_unpack reads, and (lanes of lane group 0) the two fp16 scales of its row
+// at qs[((nt * KCw + kc) * 16 + row) * 2 + block].
+template <typename ST>
+__global__ void __launch_bounds__(256)
+pack_q4_kernel(PackSrc p, int n_tiles, int KCw, u32x2_t* out, uint16_t* qs) {
+    const size_t u = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t total = (size_t)n_tiles * KCw * 64;
+    if (u >= total) return;
+    const int lane = (int)(u & 63);
+    const size_t ch = u >> 6;
+    const int kc = (int)(ch % KCw);
+    const int nt = (int)(ch / KCw);
+    const int r = nt * 16 + (lane & 15), g = lane >> 4;
+    int row = 0;
+    const ST* src = (const ST*)src_row(p, r, row);
+    u32x2_t v = {0x88888888u, 0x88888888u};     // padding rows: code 8 = weight 0
+    uint16_t sc[2] = {0, 0};
+    if (src != nullptr) {
+        const ST* s = src + (size_t)row * p.K;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int k0 = kc * 64 + 32 * h;
+            float d, inv;
+            q4_block<ST>(s, k0, p.K, d, inv);
+            uint32_t w = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int k = k0 + 8 * g + e;
+                const float x = (k < p.K) ? to_f32<ST>(s[k]) : 0.f;
+                w |= q4_code(x, inv) << ((e & 1) ? 16 + 4 * (e >> 1) : 4 * (e >> 1));
+            }
+            v[h] = w;
+            sc[h] = f32_to_f16_bits(d);
+        }
+    }
+    out[u] = v;
+    if (g == 0) *(uint32_t*)(qs + ((size_t)(nt * KCw + kc) * 16 + (lane & 15)) * 2) = sc[0] | ((uint32_t)sc[1] << 16);
+}
+
+// Q4_0 quantisation to plain row-major arrays (the converter's output, and the
+// form the quantiser is checked in): one thread per (row, 32-column block);
+// codes [rows][nb * 32] one byte each (padding columns quantised as 0), scales
+// [rows][nb] fp16 bits.
+template <typename ST>
+__global__ void __launch_bounds__(256)
+quantize_q4_kernel(const ST* w, int rows, int K, uint8_t* codes, uint16_t* scales) {
+    const int nb = (K + 31) / 32;
+    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)rows * nb) return;
+    const int r = (int)(t / nb), b = (int)(t % nb);
+    const ST* s = w + (size_t)r * K;
+    float d, inv;
+    q4_block<ST>(s, 32 * b, K, d, inv);
+    for (int e = 0; e < 32; ++e) {
+        const int k = 32 * b + e;
+        codes[(size_t)r * nb * 32 + k] = (uint8_t)q4_code((k < K) ? to_f32<ST>(s[k]) : 0.f, inv);
+    }
+    scales[(size_t)r * nb + b] = f32_to_f16_bits(d);
+}
+
 // Per packed row: s = max |w| / 127 (fp32, correctly rounded division).
 template <typename ST>
 __global__ void __launch_bounds__(256) row_scale_kernel(PackSrc p, int n_rows_padded, float* scale) {

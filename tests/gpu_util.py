@@ -19,7 +19,7 @@ def build_pair(shape, dtype: str, max_window: int = 64, max_pos: int = 1024, see
     w = synth.all_weights(shape, weight_dtype(dtype), seed)
     model = dl.Model(shape, dtype, {k: w[k] for k in GLOBALS}, lambda l: w["layers"][l],
                      max_window=max_window, max_pos=max_pos)
-    om = oracle.OracleModel(shape, w, int8=(dtype == "w8")) if oracle_too else None
+    om = oracle.OracleModel(shape, w, int8=(dtype == "w8"), q4=(dtype == "q4")) if oracle_too else None
     return model, om, w
 
 

@@ -36,7 +36,8 @@ def _run(shape, dtype, P, W, masked, cap_extra=0):
     logits, ids, conf = gpu_logits(model, kv, tok, mask)
     s_ids, s_conf = gpu_step(model, kv, tok, mask)
     print("  gpu done; oracle ...", flush=True)
-    om = oracle.OracleModel(shape, dict(glob, layers=layers), int8=(dtype == "w8"), cache_layers=False)
+    om = oracle.OracleModel(shape, dict(glob, layers=layers), int8=(dtype == "w8"), q4=(dtype == "q4"),
+                            cache_layers=False)
     okv = oracle.OracleKV(shape, P + W + cap_extra)
     oracle.prefill(om, okv, prompt)
     ref = oracle.denoise_step(om, okv, tok, mask)
@@ -53,7 +54,8 @@ def _run(shape, dtype, P, W, masked, cap_extra=0):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("dtype,P,W", [("bf16", 512, 32), ("bf16", 512, 48), ("bf16", 1024, 64), ("w8", 512, 64)])
+@pytest.mark.parametrize("dtype,P,W", [("bf16", 512, 32), ("bf16", 512, 48), ("bf16", 1024, 64), ("w8", 512, 64),
+                                       ("q4", 512, 32), ("q4", 512, 64)])
 def test_8b_width_two_layers(dtype, P, W):
     masked = list(range(8, 32)) if W == 32 else list(range(24, W))
     _run(BIG.with_layers(2), dtype, P, W, masked)
