@@ -61,6 +61,16 @@ def test_8b_width_two_layers(dtype, P, W):
     _run(BIG.with_layers(2), dtype, P, W, masked)
 
 
+@pytest.mark.timeout(900)
+def test_8b_width_long_prefix_int8_spec_window():
+    """The long-prefix int8 speculative launch configuration at the 8B widths: int8
+    weights, a 64-row window, and a prefix long enough that the attention's key
+    splits hit their cap (2048 keys: 66 blocks in 14 splits; the 4096-key workload
+    takes 15 splits through the same code).  One layer: the oracle's prefill is the
+    cost."""
+    _run(BIG.with_layers(1), "w8", 2048, 64, list(range(0, 64)))
+
+
 @pytest.mark.slow
 @pytest.mark.timeout(900)
 def test_8b_full_depth_step():

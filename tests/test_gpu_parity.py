@@ -101,7 +101,7 @@ def test_tiny_generation_with_resync(tiny):
     kv.close()
 
 
-@pytest.mark.parametrize("W", [1, 5, 16, 31, 33, 40, 48, 49, 64, 100])
+@pytest.mark.parametrize("W", [1, 5, 16, 31, 33, 40, 48, 49, 64, 100, 256])
 def test_micro_window_sizes(micro, W):
     model, om = micro
     sh = synth.MICRO
@@ -129,6 +129,26 @@ def test_small_lowp_step(small, W):
     assert_ids_match_where_decided(ids, ref.logits, err)
     np.testing.assert_allclose(conf, ref.conf, rtol=0.1)
     kv.close()
+
+
+def test_small_bf16_max_window_and_long_prefill():
+    """The largest window a model allows (max_window = 256: four 64-row token blocks
+    per launch) and a 1000-token prompt (16 token blocks, ragged), bf16."""
+    sh = SMALL
+    model, om, _ = build_pair(sh, "bf16", max_window=256, max_pos=1400)
+    P0, W = 1000, 256
+    print(f"case: small bf16 prefill {P0}, window {W}", flush=True)
+    kv, okv, prompt = _prefilled(model, om, sh, P0, P0 + W)
+    allowed = oracle.block_causal_allowed(P0, P0, sh.block)
+    _, _, K, V = oracle.forward_full(om, prompt, allowed)
+    _cache_vs(kv, K, V, P0, 3e-2, 3e-2)
+    tok, mask = synth.window(sh, W, range(0, W, 3))
+    logits, ids, conf = gpu_logits(model, kv, tok, mask)
+    ref = oracle.denoise_step(om, okv, tok, mask)
+    err = assert_logits_close(logits, ref.logits, tol("bf16"))
+    assert_ids_match_where_decided(ids, ref.logits, err)
+    kv.close()
+    model.close()
 
 
 def _cache_vs(kv, K_ref, V_ref, n, atol, rtol):
