@@ -301,6 +301,19 @@ int dllm_probe_enable(dllm_model* m, int32_t kernel_class, int32_t max_records);
  * (milliseconds) of the recorded launches; resets the record count. */
 int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms);
 
+/* Kernel timing by replay: issues, back to back on `stream`, n_launches launches of
+ * one kernel class exactly as a denoising step over W rows at prefix P = prefix_len
+ * issues them (same kernels, launch shapes and operands), layer 0, 1, ... cyclically
+ * (the LM head: the same launch n_launches times).  The caller brackets the call
+ * with events; elapsed / n_launches is the class's mean launch duration without
+ * per-launch event records.  The operands are whatever the model's workspaces
+ * hold (run a step first for realistic values); the launches overwrite those
+ * workspaces and the cache rows [P, P + W) of every layer, which are step scratch,
+ * and nothing else.  E_INVAL for an unknown class, W outside [1, max_window] or
+ * n_launches < 1; E_CAPACITY if P + W > capacity. */
+int dllm_kernel_replay(dllm_model* m, dllm_kv* kv, int32_t kernel_class, int32_t W, int32_t n_launches,
+                       dllm_stream stream);
+
 /* Algorithmic bytes one launch of a kernel class moves for a window of W rows at
  * prefix P (weights once, KV read, KV written, activations; no logits).  Used to
  * express achieved bandwidth. */

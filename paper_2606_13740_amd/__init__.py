@@ -75,6 +75,7 @@ _SIGNATURES = {
     "dllm_probe_enable": ([_vp, _i32, _i32], ctypes.c_int),
     "dllm_probe_read": ([_vp, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dllm_kernel_bytes": ([_vp, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "dllm_kernel_replay": ([_vp, _vp, _i32, _i32, _i32, _vp], ctypes.c_int),
     "dllm_read_bandwidth": ([_vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
     "dllm_quantize_q4_0": ([_vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_commit_staged": ([_vp, _vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_float, ctypes.c_float, _vp, _vp, _vp],
@@ -230,6 +231,10 @@ def dllm_probe_read(model: int):
     n, ms = _i32(), ctypes.c_double()
     _check(lib().dllm_probe_read(model, ctypes.byref(n), ctypes.byref(ms)), "dllm_probe_read")
     return n.value, ms.value
+
+
+def dllm_kernel_replay(model: int, kv: int, kernel_class: int, W: int, n_launches: int, stream=None):
+    _check(lib().dllm_kernel_replay(model, kv, kernel_class, W, n_launches, _stream(stream)), "dllm_kernel_replay")
 
 
 def dllm_kernel_bytes(model: int, kernel_class: int, W: int, P: int) -> float:

@@ -381,6 +381,8 @@ struct FwdArgs {
     bool sel;                 // LM head over selected rows only (selective logits skipping)
     const uint8_t* need;      // device row flags (nullable: every row) when sel
     int n_sel;                // at most this many flagged rows get an LM output
+    int replay = -1;          // >= 0: only launch this kernel class, n_replay times (timing)
+    int n_replay = 0;
 };
 
 // O / down projection: split-K GEMM into partials, then the reduction that adds
@@ -425,21 +427,28 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (a.lm && Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
     }
 
-    hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const AT*)m->embed, a.tok, a.mask,
-                       a.M, d, c.vocab, c.mask_id, c.eps, (const float*)m->layers[0].g1, w.x, w.xg, m->KCx_d);
+    // replay (timing): the kernels of one class only, with the operands the workspace
+    // holds, cycling through the layers
+    auto run = [&](int cls) { return a.replay < 0 || a.replay == cls; };
+    if (a.replay < 0)
+        hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const AT*)m->embed, a.tok,
+                           a.mask, a.M, d, c.vocab, c.mask_id, c.eps, (const float*)m->layers[0].g1, w.x, w.xg,
+                           m->KCx_d);
 
     // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo]; Hkv heads.
     const size_t plane = (size_t)m->Hkv * kv->Cs * Dh;
     const size_t layer_elems = (XF32 ? 2 : 4) * plane;
     const size_t kv_plane = XF32 ? 0 : plane;
     const size_t q_plane = XF32 ? 0 : (size_t)w.rows * d;
-    for (int l = 0; l < a.n_layers; ++l) {
+    const int n_iter = a.replay < 0 ? a.n_layers : (a.replay == DLLM_K_LMHEAD ? 0 : a.n_replay);
+    for (int it = 0; it < n_iter; ++it) {
+        const int l = it % c.n_layers;
         LayerW& L = m->layers[l];
         AT* Kc = (AT*)kv->buf + (size_t)l * layer_elems;
         AT* Vt = Kc + (XF32 ? plane : 2 * plane);
 
         // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
-        {
+        if (run(DLLM_K_QKV)) {
             GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles, L.bqkv};
             g.qs = L.qkv.qs;
             EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane,
@@ -449,7 +458,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 return rc;
         }
         // attention over [0, T) (+ split merge)
-        {
+        if (run(DLLM_K_ATTN)) {
             AttnArgs at{};
             at.q = w.q; at.q_plane = q_plane; at.K = Kc; at.Vt = Vt; at.kv_plane = kv_plane; at.Cs = kv->Cs; at.H = H;
             at.G = H / m->Hkv; at.T = a.T; at.lim = a.lim; at.M = a.M;
@@ -488,12 +497,12 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
             }
         }
         // O projection + residual (+ the norm-2 operand)
-        {
+        if (run(DLLM_K_OPROJ)) {
             ProbeScope ps(m, DLLM_K_OPROJ, s);
             if ((rc = residual_proj<WT, XF32>(m, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) return rc;
         }
         // RMSNorm + gate/up + SwiGLU
-        {
+        if (run(DLLM_K_GATEUP)) {
             GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles};
             g.qs = L.gu.qs;
             EpiSwiGLU<XF32> e{w.af, m->KCx_f};
@@ -502,7 +511,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 return rc;
         }
         // down projection + residual (+ next norm operand)
-        {
+        if (run(DLLM_K_DOWN)) {
             const bool last = (l + 1 == c.n_layers);
             const float* gnext = last ? m->gf : m->layers[l + 1].g1;
             const bool sel = last && a.lm && a.sel;
@@ -512,7 +521,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         }
     }
     if (a.xout) HIP_TRY(hipMemcpyAsync(a.xout, w.x, (size_t)a.M * d * 4, hipMemcpyDeviceToDevice, s));
-    if (a.lm) {
+    if (a.lm || a.replay == DLLM_K_LMHEAD) {
         // rows the LM head runs over: all M, or the selected ones packed to the front
         const int Ml = a.sel ? std::min(a.n_sel, a.M) : a.M;
         int MTl = MT, gyl = gy;
@@ -528,11 +537,14 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (gx > m->n_lm_wg) return fail(DLLM_E_INVAL, "internal: LM-head partials exceed their buffer");
         if (Ml > 0) {
             EpiLM e{c.vocab, c.mask_id, Ml, w.lm, w.wrows, a.logits};
-            ProbeScope ps(m, DLLM_K_LMHEAD, s);
-            if ((rc = launch_gemm<WT, G_LM>(dc, m->lm.n_tiles, MTl, g, e, gyl, s))) return rc;
+            for (int r = 0; r < (a.replay < 0 ? 1 : a.n_replay); ++r) {
+                ProbeScope ps(m, DLLM_K_LMHEAD, s);
+                if ((rc = launch_gemm<WT, G_LM>(dc, m->lm.n_tiles, MTl, g, e, gyl, s))) return rc;
+            }
         }
-        hipLaunchKernelGGL(lm_combine_kernel, dim3(a.M), dim3(64), 0, s, (const LmPartial*)w.lm, gx, w.wrows,
-                           a.out_id, a.out_conf, a.sel, a.need, a.n_sel, a.M);
+        if (a.replay < 0)
+            hipLaunchKernelGGL(lm_combine_kernel, dim3(a.M), dim3(64), 0, s, (const LmPartial*)w.lm, gx, w.wrows,
+                               a.out_id, a.out_conf, a.sel, a.need, a.n_sel, a.M);
     }
     HIP_TRY(hipGetLastError());
     return DLLM_OK;
@@ -967,6 +979,20 @@ int dllm_probe_read(dllm_model* m, int32_t* n_records, double* mean_ms) {
     *mean_ms = m->probe_n ? tot / m->probe_n : 0.0;
     m->probe_n = 0;
     return DLLM_OK;
+}
+
+int dllm_kernel_replay(dllm_model* m, dllm_kv* kv, int32_t kernel_class, int32_t W, int32_t n_launches,
+                       dllm_stream stream) {
+    int rc = check_model_kv(m, kv);
+    if (rc) return rc;
+    if (kernel_class < 0 || kernel_class > DLLM_K_LMHEAD) return fail(DLLM_E_INVAL, "unknown kernel class");
+    if (W < 1 || W > m->cfg.max_window) return fail(DLLM_E_INVAL, "W must be in [1, max_window]");
+    if (n_launches < 1) return fail(DLLM_E_INVAL, "n_launches must be >= 1");
+    if (kv->prefix_len + W > kv->capacity) return fail(DLLM_E_CAPACITY, "prefix_len + W exceeds the capacity");
+    FwdArgs a{};
+    a.M = W; a.tok = nullptr; a.mask = nullptr; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + W;
+    a.n_layers = m->cfg.n_layers; a.lm = false; a.replay = kernel_class; a.n_replay = n_launches;
+    return forward(m, kv, a, (hipStream_t)stream);
 }
 
 int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes) {

@@ -106,6 +106,7 @@ def test_null_handles_are_rejected(dl):
                               None) == dl.DLLM_E_INVAL
     assert L.dllm_denoise_window(None, None, 0, None, None, 32, None, None, None) == dl.DLLM_E_INVAL
     assert L.dllm_denoise_window_sls(None, None, 0, None, None, None, 0, 32, None, None, None) == dl.DLLM_E_INVAL
+    assert L.dllm_kernel_replay(None, None, 0, 32, 1, None) == dl.DLLM_E_INVAL
 
 
 def test_draft_calls_validate_on_host(dl):

@@ -264,6 +264,29 @@ def test_step_is_deterministic_and_matches_debug(small):
     kv.close()
 
 
+def test_kernel_replay_leaves_the_prefix_and_later_steps_unchanged(small):
+    """dllm_kernel_replay (timing) relaunches the step's kernels on workspace and
+    window scratch only: the prefix cache stays bit-identical and the next step
+    gives bit-identical outputs."""
+    model, om, dtype = small
+    sh = SMALL
+    kv, okv, _ = _prefilled(model, om, sh, 70, 70 + 32)
+    tok, mask = synth.window(sh, 32, range(8, 32))
+    ids0, conf0 = gpu_step(model, kv, tok, mask)
+    K0, V0 = kv.views()
+    for cls in range(6):
+        dl.dllm_kernel_replay(model.handle, kv.handle, cls, 32, 5)
+    torch.cuda.synchronize()
+    K1, V1 = kv.views()
+    assert torch.equal(K0[:, :, :70], K1[:, :, :70]) and torch.equal(V0[:, :, :, :70], V1[:, :, :, :70])
+    ids1, conf1 = gpu_step(model, kv, tok, mask)
+    np.testing.assert_array_equal(ids0, ids1)
+    np.testing.assert_array_equal(conf0, conf1)
+    with pytest.raises(dl.DllmError):
+        dl.dllm_kernel_replay(model.handle, kv.handle, 6, 32, 1)
+    kv.close()
+
+
 def test_window_never_touches_prefix(small):
     """A step (drafts included) leaves cache rows [0, P) and prefix_len unchanged."""
     model, om, dtype = small
