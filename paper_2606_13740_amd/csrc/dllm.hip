@@ -163,10 +163,11 @@ struct Decomp {
 
 constexpr int N_CU = 256;
 
-// Q4_0 gate/up keeps 4 tiles: at 6 its two-stage pipeline of codes, scales and hi/lo
-// activations does not fit 256 VGPRs.
+// Q4_0 gate/up keeps 3 tiles: at 6 its code pipeline and hi/lo activations do not fit
+// 256 VGPRs, and every template slot is computed, so the 3 tiles per wave group the
+// LLaDA-8B gate/up takes (512 workgroups) should fill it.
 constexpr int template_fw(GemmKind k, int wt) {
-    return k == G_QKV ? 3 : (k == G_GU ? (wt == WT_Q4 ? 4 : 6) : (k == G_LM ? 8 : 4));
+    return k == G_QKV ? 3 : (k == G_GU ? (wt == WT_Q4 ? 3 : 6) : (k == G_LM ? 8 : 4));
 }
 int template_nwn(GemmKind k) { return k == G_LM ? 4 : 1; }
 

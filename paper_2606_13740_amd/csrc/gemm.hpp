@@ -52,14 +52,30 @@ template <int WT, int F, int MT>
 constexpr int pipeline_depth() {
     constexpr int XP = (WT == WT_F32) ? 1 : 2;
     if constexpr (WT == WT_Q4) {
-        // 8-byte code loads + a scale dword per tile, 16 activation dwords per token
-        // tile: two stages up to 2 token tiles, one beyond (the accumulators of 3-4
-        // token tiles leave no room for a second)
-        return MT <= 2 ? 2 : 1;
+        // code stages: 8-byte codes + a scale dword per tile (3 VGPRs); the
+        // activations have their own, shallower pipeline (activation_depth), so the
+        // codes can run deeper: ~64 VGPRs of them up to 2 token tiles (an even count,
+        // a multiple of the activation depth), ~36 at 3 and one stage at 4 token tiles
+        if constexpr (MT <= 2) {
+            constexpr int d = 64 / (3 * F);
+            return d < 2 ? 2 : (d > 8 ? 8 : (d & ~1));
+        } else {
+            constexpr int d = (MT == 3 ? 36 : 12) / (3 * F);
+            return d < 1 ? 1 : (d > 8 ? 8 : d);
+        }
     }
     constexpr int slot = 4 * (F + MT * WTraits<WT>::XPER * XP);
     constexpr int d = 128 / slot;
     return d < 1 ? 1 : (d > 8 ? 8 : d);
+}
+
+// Activation stages in flight: the weight depth, except for Q4_0 whose code
+// pipeline runs deeper than its activations (L2-resident, 16 dwords per token tile
+// and stage): two stages up to 2 token tiles, one beyond.
+template <int WT, int F, int MT>
+constexpr int activation_depth() {
+    if constexpr (WT == WT_Q4) return MT <= 2 ? 2 : 1;
+    return pipeline_depth<WT, F, MT>();
 }
 
 // Reduction slots: the largest power of two <= NWk whose slots fit the budget.
@@ -83,6 +99,8 @@ gemm_kernel(GemmArgs g, Epi epi) {
     constexpr int XP = XF ? 1 : 2;                 // activation planes (hi, lo)
     constexpr int XB = XChunk<XF>::bytes;
     constexpr int D = pipeline_depth<WT, FW, MT>();
+    constexpr int DX = activation_depth<WT, FW, MT>();
+    static_assert(D % DX == 0, "activation stages must divide the weight stages");
     constexpr int NW = NWn * NWk;
     constexpr int NR = 16 * FW, MR = 16 * MT, LDY = MR + 1;
     // K-slice partials: S slots per row group (S <= NWk, a power of two that keeps
@@ -142,9 +160,9 @@ gemm_kernel(GemmArgs g, Epi epi) {
         u32x4_t wb[D][FW];                    // weight chunks (bf16 / int8 / fp32)
         [[maybe_unused]] u32x2_t wq[D][FW];   // Q4_0 codes
         [[maybe_unused]] uint32_t wsc[D][FW]; // Q4_0 scales (two fp16)
-        u32x4_t xb[D][MT * XPER * XP];
+        u32x4_t xb[DX][MT * XPER * XP];
 
-        auto load = [&](int s, int c) {
+        auto loadw = [&](int s, int c) {
 #pragma unroll
             for (int f = 0; f < FW; ++f) {
                 if (f >= nf) continue;
@@ -155,6 +173,8 @@ gemm_kernel(GemmArgs g, Epi epi) {
                     wb[s][f] = ldg16_nt(wp + f * wtile + (size_t)c * WCB);
                 }
             }
+        };
+        auto loadx = [&](int s, int c) {
 #pragma unroll
             for (int t = 0; t < MT; ++t)
 #pragma unroll
@@ -164,7 +184,7 @@ gemm_kernel(GemmArgs g, Epi epi) {
                         xb[s][(t * XPER + h) * XP + pl] =
                             ldg16(xp + t * xtile + (size_t)(c * XPER + h) * XB + pl * 1024);
         };
-        auto compute = [&](int s) {
+        auto compute = [&](int s, int sx) {
             // Q4_0 (weights as the B operand, so a lane's accumulator column is one
             // weight row and takes one scale per block): codes unpack to bf16 128 + q,
             // so a block's MFMAs start from zp = -136 * sum_k x and give
@@ -176,20 +196,19 @@ gemm_kernel(GemmArgs g, Epi epi) {
                     f32x4_t zp[MT];
 #pragma unroll
                     for (int t = 0; t < MT; ++t) {
-                        f32x4_t z = mfma_bf16(xb[s][(t * 2 + h) * 2 + 0], ones, f32x4_t{0.f, 0.f, 0.f, 0.f});
-                        z = mfma_bf16(xb[s][(t * 2 + h) * 2 + 1], ones, z);
+                        f32x4_t z = mfma_bf16(xb[sx][(t * 2 + h) * 2 + 0], ones, f32x4_t{0.f, 0.f, 0.f, 0.f});
+                        z = mfma_bf16(xb[sx][(t * 2 + h) * 2 + 1], ones, z);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) zp[t][i] = -136.0f * z[i];
                     }
 #pragma unroll
                     for (int f = 0; f < FW; ++f) {
-                        if (f >= nf) continue;
                         const float sc = f16_bits_to_f32(h == 0 ? (wsc[s][f] & 0xFFFFu) : (wsc[s][f] >> 16));
                         const u32x4_t w = q4_unpack(wq[s][f][h]);
 #pragma unroll
                         for (int t = 0; t < MT; ++t) {
-                            f32x4_t v = mfma_bf16(xb[s][(t * 2 + h) * 2 + 0], w, zp[t]);
-                            v = mfma_bf16(xb[s][(t * 2 + h) * 2 + 1], w, v);
+                            f32x4_t v = mfma_bf16(xb[sx][(t * 2 + h) * 2 + 0], w, zp[t]);
+                            v = mfma_bf16(xb[sx][(t * 2 + h) * 2 + 1], w, v);
 #pragma unroll
                             for (int i = 0; i < 4; ++i) acc[f][t][i] = fmaf(sc, v[i], acc[f][t][i]);
                         }
@@ -199,48 +218,66 @@ gemm_kernel(GemmArgs g, Epi epi) {
             }
 #pragma unroll
             for (int f = 0; f < FW; ++f) {
-                if (f >= nf) continue;
                 if constexpr (WT == WT_BF16) {
 #pragma unroll
                     for (int t = 0; t < MT; ++t) {
-                        acc[f][t] = mfma_bf16(wb[s][f], xb[s][t * 2 + 0], acc[f][t]);
-                        acc[f][t] = mfma_bf16(wb[s][f], xb[s][t * 2 + 1], acc[f][t]);
+                        acc[f][t] = mfma_bf16(wb[s][f], xb[sx][t * 2 + 0], acc[f][t]);
+                        acc[f][t] = mfma_bf16(wb[s][f], xb[sx][t * 2 + 1], acc[f][t]);
                     }
                 } else if constexpr (WT == WT_I8) {
                     const u32x4_t w0 = i8x8_to_bf16x8(wb[s][f][0], wb[s][f][1]);
                     const u32x4_t w1 = i8x8_to_bf16x8(wb[s][f][2], wb[s][f][3]);
 #pragma unroll
                     for (int t = 0; t < MT; ++t) {
-                        acc[f][t] = mfma_bf16(w0, xb[s][(t * 2 + 0) * 2 + 0], acc[f][t]);
-                        acc[f][t] = mfma_bf16(w0, xb[s][(t * 2 + 0) * 2 + 1], acc[f][t]);
-                        acc[f][t] = mfma_bf16(w1, xb[s][(t * 2 + 1) * 2 + 0], acc[f][t]);
-                        acc[f][t] = mfma_bf16(w1, xb[s][(t * 2 + 1) * 2 + 1], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w0, xb[sx][(t * 2 + 0) * 2 + 0], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w0, xb[sx][(t * 2 + 0) * 2 + 1], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w1, xb[sx][(t * 2 + 1) * 2 + 0], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w1, xb[sx][(t * 2 + 1) * 2 + 1], acc[f][t]);
                     }
                 } else {
 #pragma unroll
                     for (int t = 0; t < MT; ++t)
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
-                            acc[f][t] = mfma_f32(__uint_as_float(wb[s][f][q]), __uint_as_float(xb[s][t][q]),
+                            acc[f][t] = mfma_f32(__uint_as_float(wb[s][f][q]), __uint_as_float(xb[sx][t][q]),
                                                  acc[f][t]);
                 }
             }
         };
 
+        // Every tile slot of the template is computed, without a per-tile branch (a
+        // branch per tile splits the unrolled step into basic blocks the scheduler
+        // cannot interleave); slots past nf hold zeros (never loaded) and their
+        // results are never stored.
+#pragma unroll
+        for (int s = 0; s < D; ++s)
+#pragma unroll
+            for (int f = 0; f < FW; ++f) {
+                if constexpr (WT == WT_Q4) {
+                    wq[s][f] = u32x2_t{0u, 0u};
+                    wsc[s][f] = 0u;
+                } else {
+                    wb[s][f] = u32x4_t{0u, 0u, 0u, 0u};
+                }
+            }
         const bool work = c1 > c0 && nf > 0;
         if (work) {
 #pragma unroll
-            for (int s = 0; s < D; ++s) load(s, min(c0 + s, c1 - 1));
+            for (int s = 0; s < D; ++s) {
+                loadw(s, min(c0 + s, c1 - 1));
+                if (s < DX) loadx(s, min(c0 + s, c1 - 1));
+            }
         }
         stage_prologue();
         if (work) {
+            // chunk c uses weight slot c % D and activation slot c % DX (DX divides D)
             for (int base = c0; base < c1; base += D) {
 #pragma unroll
                 for (int s = 0; s < D; ++s) {
-                    const int c = base + s;
-                    if (c < c1) compute(s);
-                    const int cn = c + D;
-                    if (cn < c1) load(s, cn);
+                    const int c = base + s, sx = s % DX;
+                    if (c < c1) compute(s, sx);
+                    if (c + D < c1) loadw(s, c + D);
+                    if (c + DX < c1) loadx(sx, c + DX);
                 }
             }
         }
