@@ -203,6 +203,11 @@ gemm_kernel(GemmArgs g, Epi epi) {
                     }
 #pragma unroll
                     for (int f = 0; f < FW; ++f) {
+                        // at 3-4 token tiles the Q4_0 chains of all tiles do not fit the
+                        // registers together: one tile at a time
+                        if constexpr (MT >= 3) {
+                            if (f >= nf) continue;
+                        }
                         const float sc = f16_bits_to_f32(h == 0 ? (wsc[s][f] & 0xFFFFu) : (wsc[s][f] >> 16));
                         const u32x4_t w = q4_unpack(wq[s][f][h]);
 #pragma unroll
