@@ -151,10 +151,11 @@ int pick_MT(int M) {
 // (tpg) and fewer split-K slices (ks).  Every workgroup of these layouts holds a
 // whole CU (8 waves at ~200 VGPRs, or 100+ KiB of LDS), so a launch of more than
 // 256 workgroups runs in rounds: (tpg, ks) is chosen to minimise the busiest CU's
-// share, rounds x tpg / ks row tiles of full K, which picks the layouts above at
-// the LLaDA-8B widths (256 or 247 workgroups) and e.g. 5 tiles per wave group for
-// the Dream-7B gate/up and LM head.  Small models (fewer row tiles than the
-// thresholds below) use one tile per 4-wave workgroup.
+// share, rounds x (tpg / ks + 1) row tiles of full K, the 1 standing for a
+// workgroup's fixed cost (start-up, K-slice reduction, epilogue); this picks the
+// layouts above at the LLaDA-8B widths (256 or 247 workgroups) and e.g. 5 tiles
+// per wave group for the Dream-7B gate/up and LM head.  Small models (fewer row
+// tiles than the thresholds below) use one tile per 4-wave workgroup.
 struct Decomp {
     bool small;   // 1 tile per workgroup of 4 waves, K over the waves
     int tpg;      // row tiles per wave group
@@ -180,7 +181,11 @@ Decomp decomp(GemmKind k, int wt, int n_tiles, int Mc, int gy) {
     for (int tpg = fw; tpg >= 1; --tpg) {
         for (int ks = (k == G_RES && Mc <= 64) ? RES_SPLIT : 1; ks >= 1; ks >>= 1) {
             const long wgs = (long)ceil_div(ceil_div(n_tiles, tpg), nwn) * ks * gy;
-            const double load = (double)ceil_div(wgs, N_CU) * tpg / ks;
+            // busiest CU: rounds x (its tiles of full K + a workgroup's fixed cost, about
+            // one tile).  Every template slot's MFMAs run whether or not the group fills
+            // it, so past 2 token tiles a group costs at least half the template.
+            const double work = Mc > 32 ? std::max<double>(tpg, fw / 2.0) : (double)tpg;
+            const double load = (double)ceil_div(wgs, N_CU) * (work / ks + 1.0);
             if (load < best_load - 1e-9) { best_load = load; best = Decomp{false, tpg, ks}; }
         }
     }
