@@ -164,18 +164,21 @@ struct Decomp {
 
 constexpr int N_CU = 256;
 
-// Q4_0 gate/up keeps 3 tiles: at 6 its code pipeline and hi/lo activations do not fit
-// 256 VGPRs, and every template slot is computed, so the 3 tiles per wave group the
-// LLaDA-8B gate/up takes (512 workgroups) should fill it.
-constexpr int template_fw(GemmKind k, int wt) {
-    return k == G_QKV ? 3 : (k == G_GU ? (wt == WT_Q4 ? 3 : 6) : (k == G_LM ? 8 : 4));
+// Row tiles per wave group of each template at mt token tiles.  Q4_0 exceptions:
+// the LM head takes 4, since at 8 its code pipeline, activations and 16
+// accumulators per token tile need more than 256 registers and leave one wave per
+// SIMD (LLaDA-8B vocabulary at 32 rows: 119 against 144 us per launch); the
+// gate/up takes 3 past 2 token tiles, where 6 would spill.
+constexpr int template_fw(GemmKind k, int wt, int mt) {
+    if (wt == WT_Q4 && k == G_GU && mt >= 3) return 3;
+    return k == G_QKV ? 3 : (k == G_GU ? 6 : (k == G_LM ? (wt == WT_Q4 ? 4 : 8) : 4));
 }
 int template_nwn(GemmKind k) { return k == G_LM ? 4 : 1; }
 
 Decomp decomp(GemmKind k, int wt, int n_tiles, int Mc, int gy) {
     const int min_tiles = (k == G_QKV || k == G_RES) ? 128 : (k == G_GU ? 256 : 512);
     if (n_tiles < min_tiles) return Decomp{true, 1, 1};
-    const int fw = template_fw(k, wt), nwn = template_nwn(k);
+    const int fw = template_fw(k, wt, Mc / (16 * gy)), nwn = template_nwn(k);
     Decomp best{false, 1, 1};
     double best_load = 1e30;
     for (int tpg = fw; tpg >= 1; --tpg) {
@@ -198,15 +201,21 @@ void launch_gemm_inst(const GemmArgs& g, const Epi& epi, int n_tiles, int KS, in
     hipLaunchKernelGGL((gemm_kernel<WT, FW, NWn, NWk, MT, Epi>), grid, dim3(NWn * NWk * 64), 0, s, g, epi);
 }
 
-template <int WT, int FW, int NWn, int NWk, class Epi>
+// Row tiles of kind KIND_FW's template at mt token tiles; KIND_FW < 0 is the
+// small-model layout (one tile).
+template <int WT, int KIND_FW>
+constexpr int fw_of(int mt) { return KIND_FW < 0 ? 1 : template_fw((GemmKind)KIND_FW, WT, mt); }
+
+template <int WT, int KIND_FW, int NWn, int NWk, class Epi>
 int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int KS, int gy, hipStream_t s) {
-    if (g.tpg < 1 || g.tpg > FW) return fail(DLLM_E_INVAL, "internal: row tiles per group outside the template");
+    constexpr auto fw = fw_of<WT, KIND_FW>;
+    if (MT < 1 || MT > 4) return fail(DLLM_E_UNIMPL, "unsupported token tile count");
+    if (g.tpg < 1 || g.tpg > fw(MT)) return fail(DLLM_E_INVAL, "internal: row tiles per group outside the template");
     switch (MT) {
-        case 1: launch_gemm_inst<WT, FW, NWn, NWk, 1>(g, epi, n_tiles, KS, gy, s); break;
-        case 2: launch_gemm_inst<WT, FW, NWn, NWk, 2>(g, epi, n_tiles, KS, gy, s); break;
-        case 3: launch_gemm_inst<WT, FW, NWn, NWk, 3>(g, epi, n_tiles, KS, gy, s); break;
-        case 4: launch_gemm_inst<WT, FW, NWn, NWk, 4>(g, epi, n_tiles, KS, gy, s); break;
-        default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
+        case 1: launch_gemm_inst<WT, fw(1), NWn, NWk, 1>(g, epi, n_tiles, KS, gy, s); break;
+        case 2: launch_gemm_inst<WT, fw(2), NWn, NWk, 2>(g, epi, n_tiles, KS, gy, s); break;
+        case 3: launch_gemm_inst<WT, fw(3), NWn, NWk, 3>(g, epi, n_tiles, KS, gy, s); break;
+        default: launch_gemm_inst<WT, fw(4), NWn, NWk, 4>(g, epi, n_tiles, KS, gy, s); break;
     }
     return DLLM_OK;
 }
@@ -218,11 +227,9 @@ template <int WT, GemmKind KIND, class Epi>
 int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const Epi& epi, int gy, hipStream_t s) {
     GemmArgs g = g0;
     g.tpg = dc.tpg;
-    if (dc.small) return launch_gemm_mt<WT, 1, 1, 4>(MT, g, epi, n_tiles, dc.ks, gy, s);
-    if constexpr (KIND == G_QKV) return launch_gemm_mt<WT, 3, 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
-    else if constexpr (KIND == G_GU) return launch_gemm_mt<WT, template_fw(G_GU, WT), 1, 8>(MT, g, epi, n_tiles, 1, gy, s);
-    else if constexpr (KIND == G_LM) return launch_gemm_mt<WT, 8, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
-    else return launch_gemm_mt<WT, 4, 1, 8>(MT, g, epi, n_tiles, dc.ks, gy, s);
+    if (dc.small) return launch_gemm_mt<WT, -1, 1, 4>(MT, g, epi, n_tiles, dc.ks, gy, s);
+    if constexpr (KIND == G_LM) return launch_gemm_mt<WT, G_LM, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
+    else return launch_gemm_mt<WT, KIND, 1, 8>(MT, g, epi, n_tiles, KIND == G_RES ? dc.ks : 1, gy, s);
 }
 
 // ---------------------------------------------------------------------------

@@ -54,8 +54,8 @@ constexpr int pipeline_depth() {
     if constexpr (WT == WT_Q4) {
         // code stages: 8-byte codes + a scale dword per tile (3 VGPRs); the
         // activations have their own, shallower pipeline (activation_depth), so the
-        // codes can run deeper: ~64 VGPRs of them up to 2 token tiles (an even count,
-        // a multiple of the activation depth), ~36 at 3 and one stage at 4 token tiles
+        // codes can run deeper: ~64 VGPRs of them up to 2 token tiles (an even count),
+        // ~36 at 3 and one stage at 4 token tiles
         if constexpr (MT <= 2) {
             constexpr int d = 64 / (3 * F);
             return d < 2 ? 2 : (d > 8 ? 8 : (d & ~1));
@@ -71,10 +71,12 @@ constexpr int pipeline_depth() {
 
 // Activation stages in flight: the weight depth, except for Q4_0 whose code
 // pipeline runs deeper than its activations (L2-resident, 16 dwords per token tile
-// and stage): two stages up to 2 token tiles, one beyond.
+// and stage): one stage, which leaves the registers for 6 row tiles per wave
+// (LLaDA-8B gate/up at 32 rows: 23.6 us per launch against 33.5 with 3 tiles and
+// two activation stages).
 template <int WT, int F, int MT>
 constexpr int activation_depth() {
-    if constexpr (WT == WT_Q4) return MT <= 2 ? 2 : 1;
+    if constexpr (WT == WT_Q4) return 1;
     return pipeline_depth<WT, F, MT>();
 }
 
