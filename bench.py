@@ -46,6 +46,9 @@ E2E = "llada8b_bf16_e2e128"      # end-to-end 128-token generation (prefill incl
 E2E_STAGED = "llada8b_bf16_e2e128_staged"   # the same with staged token stabilisation
 E2E_MERGED = "llada8b_bf16_e2e128_merged"   # the same with append + refresh piggybacked on the next step
 E2E_MBSD = "llada8b_bf16_e2e128_mbsd"       # the same with multi-block speculative decoding
+# prompt processing alone (large M: the GEMMs are MFMA-bound), bf16 and int8 weights
+PREFILL = {"llada8b_bf16_prefill512": ("bf16", 512), "llada8b_w8_prefill4096": ("w8", 4096)}
+MFMA_PEAK_TFLOPS = 2500.0        # bf16 dense
 
 
 def run_e2e(args, dl, torch, shape, dev):
@@ -332,6 +335,86 @@ def run_e2e_mbsd(args, dl, torch, shape, dev):
     }
 
 
+def run_prefill(args, dl, torch, shape, dev):
+    """dllm_prefill of a P-token prompt (all layers, no LM head), repeated: prompt
+    tokens/s.  The GEMMs multiply P rows, so they are bound by MFMA issue, not by
+    HBM: the roofline record reports the gate/up launch's algorithmic flops
+    (2 * P * 2F * d, the model's arithmetic; the hi/lo activation planes double the
+    MFMAs actually issued) against the bf16 dense MFMA peak.  Per-class durations
+    come from events around every launch of the class inside the timed prefills."""
+    dtype, P = PREFILL[args.workload]
+    glob = synth.global_weights(shape, "bf16")
+    t0 = time.time()
+    model = dl.Model(shape, dtype, glob, lambda l: synth.layer_weights(shape, l, "bf16"), max_window=64,
+                     max_pos=P + 64)
+    log(f"model created in {time.time() - t0:.1f} s")
+    kv = dl.KVCache(model, P)
+    prompt = torch.from_numpy(synth.prompt_ids(shape, P)).to(dev)
+    # a prefill needs a cache with prefix_len 0: fresh handles over the same buffer,
+    # made before the timed region (a handle is host state only)
+    pool = []
+
+    def fresh_handles(n):
+        for h in pool:
+            dl.dllm_kv_destroy(h)
+        pool[:] = [dl.dllm_kv_create(model.handle, kv.buf, kv.nbytes, P) for _ in range(n)]
+
+    def prefill():
+        dl.dllm_prefill(model.handle, pool.pop(), prompt, P)
+
+    steps = max(1, min(args.steps, 20 if P <= 512 else 5))
+    warm = max(1, min(args.warmup, 2))
+    fresh_handles(warm)
+    for _ in range(warm):
+        prefill()
+    torch.cuda.synchronize()
+    fresh_handles(steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        prefill()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    log(f"prefill {P}: {ms:.3f} ms")
+    d, F, L = shape.d_model, shape.d_ff, shape.n_layers
+    dkv = shape.kv_heads * shape.head_dim
+    flops = {"qkv": 2.0 * P * (d + 2 * dkv) * d, "oproj": 2.0 * P * d * d, "gateup": 2.0 * P * 2 * F * d,
+             "down": 2.0 * P * d * F}
+    kern = {}
+    for name, cls in dl.KERNEL_CLASSES.items():
+        if name == "lmhead":
+            continue
+        torch.cuda.synchronize()
+        fresh_handles(2)
+        dl.dllm_probe_enable(model.handle, cls, L * 2)
+        for _ in range(2):
+            prefill()
+        n, probe_ms = dl.dllm_probe_read(model.handle)
+        dl.dllm_probe_enable(model.handle, -1, 1)
+        rec = {"launches": L, "mean_us": round(probe_ms * 1e3, 2)}
+        if name in flops:
+            rec["tflops"] = round(flops[name] / (probe_ms * 1e-3) / 1e12, 1)
+        kern[name] = rec
+    torch.cuda.synchronize()
+    fresh_handles(0)
+    total_flops = L * sum(flops.values())
+    dk = kern["gateup"]
+    roof = {"bound": "mfma", "achieved": dk["tflops"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(dk["tflops"] / MFMA_PEAK_TFLOPS, 4), "traffic": None, "kernel": "gemm gate/up + SwiGLU",
+            "alg_flops_per_launch": flops["gateup"], "mean_launch_us": dk["mean_us"],
+            "timing": "HIP events around each gate/up launch inside the prefills"}
+    kv.close()
+    model.close()
+    return {"metric": f"prompt processing (prefill) tokens/sec, LLaDA-8B shape, {P}-token prompt; % of MFMA roofline",
+            "value": round(P / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warm,
+            "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": {"bf16": "bf16", "w8": "int8w-bf16a"}[dtype],
+            "data": "synthetic (seeded N(0,0.02) weights, uniform ids)",
+            "config": {"workload": args.workload, "layers": L, "d_model": d, "d_ff": F, "prompt": P},
+            "gemm_tflops": round(total_flops / (ms * 1e-3) / 1e12, 1), "kernels": kern, "roofline": roof}
+
+
 def run_sweep(args, dl, torch, shape, dev):
     """Step latency against the window's row count W (prefix 512, bf16): weight
     streaming keeps it nearly flat until the GEMMs become MFMA-bound."""
@@ -449,7 +532,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS) + [E2E, E2E_STAGED, E2E_MERGED, E2E_MBSD])
+    ap.add_argument("--workload", default=DEFAULT,
+                    choices=sorted(WORKLOADS) + [E2E, E2E_STAGED, E2E_MERGED, E2E_MBSD] + sorted(PREFILL))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sls", action="store_true",
                     help="run the LM head over every window row (no selective logits skipping)")
@@ -481,6 +565,10 @@ def main():
         run = {E2E: run_e2e, E2E_STAGED: run_e2e_staged, E2E_MERGED: run_e2e_merged,
                E2E_MBSD: run_e2e_mbsd}[args.workload]
         print(json.dumps(run(args, dl, torch, synth.LLADA_8B, torch.device("cuda:0"))), flush=True)
+        return
+    if args.workload in PREFILL:
+        torch.cuda.set_device(0)
+        print(json.dumps(run_prefill(args, dl, torch, synth.LLADA_8B, torch.device("cuda:0"))), flush=True)
         return
     if args.sweep:
         torch.cuda.set_device(0)
