@@ -160,7 +160,22 @@ struct Decomp {
     bool small;   // 1 tile per workgroup of 4 waves, K over the waves
     int tpg;      // row tiles per wave group
     int ks;       // split-K slices (residual projections)
+    bool wide = false;   // long prompts: whole-K waves of 8 row tiles (WIDE_TILES)
 };
+
+// More than 8 token blocks of 64 rows (prompts past 512 tokens, bf16 / int8
+// weights), gate/up and O/down: each wave takes 8 row tiles over the whole K range,
+// 4 row groups per workgroup sharing one token block.  The K-sliced layouts
+// re-stream every row group's weights once per token block and reach ~290 TFLOP/s
+// there; this one holds 8 x 4 tiles of accumulators per wave (LLaDA-8B, int8, 4096
+// rows: gate/up 1980 -> 1817 us, down 1156 -> 859 us, O 462 -> 371 us).  QKV keeps
+// its layout: with 2 row groups per workgroup (its RoPE staging needs the LDS) the
+// epilogue over 128 rows x 64 tokens on 128 threads made it slower (1521 -> 1688 us).
+// Up to 8 blocks the K-sliced layouts with the XCD-aware block order are faster.
+constexpr int WIDE_TILES = 8;
+bool wide_layout(GemmKind k, int wt, int gy) {
+    return gy > 8 && (k == G_GU || k == G_RES) && (wt == WT_BF16 || wt == WT_I8);
+}
 
 constexpr int N_CU = 256;
 
@@ -178,6 +193,7 @@ int template_nwn(GemmKind k) { return k == G_LM ? 4 : 1; }
 Decomp decomp(GemmKind k, int wt, int n_tiles, int Mc, int gy) {
     const int min_tiles = (k == G_QKV || k == G_RES) ? 128 : (k == G_GU ? 256 : 512);
     if (n_tiles < min_tiles) return Decomp{true, 1, 1};
+    if (wide_layout(k, wt, gy)) return Decomp{false, WIDE_TILES, 1, true};
     const int fw = template_fw(k, wt, Mc / (16 * gy)), nwn = template_nwn(k);
     Decomp best{false, 1, 1};
     double best_load = 1e30;
@@ -228,6 +244,13 @@ int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const
     GemmArgs g = g0;
     g.tpg = dc.tpg;
     if (dc.small) return launch_gemm_mt<WT, -1, 1, 4>(MT, g, epi, n_tiles, dc.ks, gy, s);
+    if constexpr ((WT == WT_BF16 || WT == WT_I8) && (KIND == G_GU || KIND == G_RES)) {
+        if (dc.wide) {
+            if (MT != 4 || g.tpg != WIDE_TILES) return fail(DLLM_E_INVAL, "internal: wide layout needs 64-row blocks");
+            launch_gemm_inst<WT, WIDE_TILES, 4, 1, 4>(g, epi, n_tiles, 1, gy, s);
+            return DLLM_OK;
+        }
+    }
     if constexpr (KIND == G_LM) return launch_gemm_mt<WT, G_LM, 4, 1>(MT, g, epi, n_tiles, 1, gy, s);
     else return launch_gemm_mt<WT, KIND, 1, 8>(MT, g, epi, n_tiles, KIND == G_RES ? dc.ks : 1, gy, s);
 }
