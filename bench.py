@@ -47,7 +47,8 @@ E2E_STAGED = "llada8b_bf16_e2e128_staged"   # the same with staged token stabili
 E2E_MERGED = "llada8b_bf16_e2e128_merged"   # the same with append + refresh piggybacked on the next step
 E2E_MBSD = "llada8b_bf16_e2e128_mbsd"       # the same with multi-block speculative decoding
 # prompt processing alone (large M: the GEMMs are MFMA-bound), bf16 and int8 weights
-PREFILL = {"llada8b_bf16_prefill512": ("bf16", 512), "llada8b_w8_prefill4096": ("w8", 4096)}
+PREFILL = {"llada8b_bf16_prefill512": ("bf16", 512), "llada8b_bf16_prefill4096": ("bf16", 4096),
+           "llada8b_w8_prefill4096": ("w8", 4096)}
 MFMA_PEAK_TFLOPS = 2500.0        # bf16 dense
 
 

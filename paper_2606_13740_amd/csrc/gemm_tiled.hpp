@@ -1,0 +1,155 @@
+// Tiled GEMM for many token rows (prompt processing): Y = X W^T with bf16 weights,
+// where the streaming kernel's waves each fetch their own operand fragments and the
+// matrix cores stay ~30% busy.
+//
+// Workgroup = 8 waves = 2 row halves x 4 token quarters; it owns 16 row tiles x 16
+// token tiles (256 rows x 256 tokens) and a K range (split-K over grid.y, for the
+// residual projections' partial sums).  Each K step (one 32-column chunk) its 16
+// weight chunks and 16 x 2 activation chunks (hi, lo planes) are copied once into
+// LDS with direct global->LDS loads, three stages deep, and every wave multiplies
+// its 8 row tiles by its 4 token tiles from there: 64 MFMAs per 16 KiB of LDS reads,
+// against 16 KiB of L1/L2 fetches per 64 MFMAs in the streaming layouts.  The
+// packed formats are the streaming kernel's (chunks are already in MFMA fragment
+// order, so an LDS chunk is read with one 16-byte load per lane).  Results go
+// through the same epilogues, in four passes of 64 tokens.
+#pragma once
+
+#include "gemm.hpp"
+
+namespace dllm {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+struct TiledShape {
+    static constexpr int RT = 16, TT = 16;   // row tiles, token tiles per workgroup
+    static constexpr int WR = 8, WM = 4;     // per wave
+    static constexpr int S = 3;              // LDS stages
+    static constexpr int WB = RT * 1024;     // weight bytes per stage
+    static constexpr int XB = TT * 2048;     // activation bytes per stage (hi + lo)
+    static constexpr int SB = WB + XB;
+    static constexpr int LOADS = (RT + 2 * TT) / 8;   // 1 KiB global->LDS loads per wave and stage
+    static constexpr int LDY = 16 * WM + 1;
+};
+
+// m_tiles: token tiles of X (its rows / 16, a multiple of 4); rows past them are
+// never read (loads clamp to the last tile) and never written.
+template <class Epi>
+__global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, int m_tiles) {
+    using T = TiledShape;
+    static_assert(T::LOADS * 8 == T::RT + 2 * T::TT, "stage loads must split evenly over the waves");
+    static_assert(16 * T::RT * T::LDY * 4 <= T::S * T::SB, "epilogue tile must fit the stage buffers");
+    __shared__ __attribute__((aligned(1024))) char sm[T::S * T::SB];
+    constexpr int ESM = Epi::kSmem > 0 ? Epi::kSmem : 16;
+    __shared__ __align__(16) char esm[ESM];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wr = wave & 1, wq = wave >> 1;
+    const int nt0 = blockIdx.x * T::RT, mt0 = blockIdx.z * T::TT;
+    const int KC = g.KCw;
+    const unsigned KS = gridDim.y;
+    const int c0 = (int)((blockIdx.y * (unsigned)KC) / KS), c1 = (int)(((blockIdx.y + 1) * (unsigned)KC) / KS);
+
+    // stage slot i: i < RT the weight chunk of row tile nt0 + i, else the activation
+    // chunk (token tile (i - RT) / 2, plane (i - RT) % 2); wave w copies slots w + 8j
+    auto stage = [&](int c, int buf) {
+        char* base = sm + buf * T::SB;
+#pragma unroll
+        for (int j = 0; j < T::LOADS; ++j) {
+            const int i = wave + 8 * j;
+            const char* src;
+            char* dst;
+            if (j < T::RT / 8) {
+                const int nt = min(nt0 + i, g.n_tiles - 1);
+                src = (const char*)g.W + (((size_t)nt * KC + c) * 64 + lane) * 16;
+                dst = base + i * 1024;
+            } else {
+                const int q = i - T::RT, tt = q >> 1, pl = q & 1;
+                const int mt = min(mt0 + tt, m_tiles - 1);
+                src = (const char*)g.X + ((size_t)mt * g.KCx + c) * 2048 + pl * 1024 + lane * 16;
+                dst = base + T::WB + tt * 2048 + pl * 1024;
+            }
+            __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)dst, 16, 0, 0);
+        }
+    };
+
+    f32x4_t acc[T::WR][T::WM];
+#pragma unroll
+    for (int f = 0; f < T::WR; ++f)
+#pragma unroll
+        for (int t = 0; t < T::WM; ++t) acc[f][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    if (c1 > c0) {
+        // every step issues one stage (past the end: the last chunk again, into a
+        // buffer nobody reads), so each wave always has exactly LOADS loads of the
+        // following stage in flight when it waits for the current one
+        stage(c0, 0);
+        stage(min(c0 + 1, c1 - 1), 1);
+        for (int c = c0; c < c1; ++c) {
+            const int cur = (c - c0) % T::S;
+            // this wave's copies of stage c have landed (the next stage's may not) and
+            // its LDS reads are done; after the barrier every wave's copies have landed
+            // and nobody reads the buffer refilled next.  (__syncthreads would also wait
+            // for the next stage's copies: the fence before its barrier waits for all
+            // outstanding vector memory operations.)
+            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(T::LOADS) : "memory");
+            stage(min(c + 2, c1 - 1), (c - c0 + 2) % T::S);
+            const char* Wb = sm + cur * T::SB;
+            const char* Xb = Wb + T::WB;
+            u32x4_t xh[T::WM], xl[T::WM];
+#pragma unroll
+            for (int t = 0; t < T::WM; ++t) {
+                xh[t] = *(const u32x4_t*)(Xb + (T::WM * wq + t) * 2048 + lane * 16);
+                xl[t] = *(const u32x4_t*)(Xb + (T::WM * wq + t) * 2048 + 1024 + lane * 16);
+            }
+#pragma unroll
+            for (int f = 0; f < T::WR; ++f) {
+                const u32x4_t w = *(const u32x4_t*)(Wb + (T::WR * wr + f) * 1024 + lane * 16);
+#pragma unroll
+                for (int t = 0; t < T::WM; ++t) {
+                    acc[f][t] = mfma_bf16(w, xh[t], acc[f][t]);
+                    acc[f][t] = mfma_bf16(w, xl[t], acc[f][t]);
+                }
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    __syncthreads();
+
+    // epilogue: four passes of 64 tokens over the stage buffers (rows 0..255 of Y)
+    float* Y = (float*)sm;
+    const int nrows = 16 * max(0, min(T::RT, g.n_tiles - nt0));
+    const int r = lane & 15, gq = lane >> 4;
+    for (int p = 0; p < T::TT / T::WM; ++p) {
+        const int mtp = mt0 + T::WM * p;
+        if (mtp >= m_tiles || nrows == 0) break;
+        const int mcols = 16 * min(T::WM, m_tiles - mtp);
+        if (wq == p) {
+#pragma unroll
+            for (int f = 0; f < T::WR; ++f)
+#pragma unroll
+                for (int t = 0; t < T::WM; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        Y[(16 * (T::WR * wr + f) + 4 * gq + i) * T::LDY + 16 * t + r] = acc[f][t][i];
+        }
+        __syncthreads();
+        if (g.wscale != nullptr || g.bias != nullptr) {
+            for (int idx = threadIdx.x; idx < nrows * mcols; idx += blockDim.x) {
+                const int n = idx / mcols, m = idx % mcols;
+                float y = Y[n * T::LDY + m];
+                if (g.wscale != nullptr) y *= g.wscale[nt0 * 16 + n];
+                if (g.bias != nullptr) y += g.bias[nt0 * 16 + n];
+                Y[n * T::LDY + m] = y;
+            }
+            __syncthreads();
+        }
+        typename Epi::Pre pre;
+        epi.fetch(pre, nt0 * 16, nrows, mtp * 16, mcols);
+        epi.stage(pre, esm, nt0 * 16, nrows, mtp * 16, mcols);
+        __syncthreads();
+        epi(Y, T::LDY, nt0 * 16, nrows, mtp * 16, mcols, blockIdx.x, esm);
+        __syncthreads();
+    }
+}
+
+}  // namespace dllm

@@ -85,6 +85,25 @@ def test_gqa_cache_equals_block_causal_recompute(pair):
     kv.close()
 
 
+def test_gqa_long_prompt_cache_equals_recompute(pair):
+    """A 300-token prompt (320 padded rows: the bf16 models take the LDS-tiled GEMM,
+    with a ragged last token tile and ragged row tiles) then one appended block."""
+    sh, dtype, model, om = pair
+    print(f"case: long prompt cache {sh.n_heads}q/{sh.kv_heads}kv {dtype}", flush=True)
+    P0 = 300
+    kv = dl.KVCache(model, P0 + sh.block)
+    prompt = synth.prompt_ids(sh, P0)
+    dl.dllm_prefill(model.handle, kv.handle, dev_i32(prompt), P0)
+    blk = synth.uniform_ids(90, 1, sh.block, sh.mask_id)
+    dl.dllm_append_prefix_kv(model.handle, kv.handle, dev_i32(blk), sh.block)
+    torch.cuda.synchronize()
+    seq = np.concatenate([prompt, blk])
+    _, _, K, V = oracle.forward_full(om, seq, oracle.block_causal_allowed(len(seq), P0, sh.block))
+    atol, rtol = (1e-5, 1e-4) if dtype == "f32" else (3e-2, 3e-2)
+    _cache_vs(kv, K, V, len(seq), atol, rtol)
+    kv.close()
+
+
 def test_gqa_refresh_matches_oracle(pair):
     sh, dtype, model, om = pair
     print(f"case: refresh {sh.n_heads}q/{sh.kv_heads}kv {dtype}", flush=True)
