@@ -167,22 +167,30 @@ struct Decomp {
 
 constexpr int N_CU = 256;
 
-// bf16 GEMMs over 256 or more token rows (prompts, wide windows) except the LM head
-// run the LDS-tiled kernel when it gives the chip at least TILED_MIN_WG workgroups:
-// every weight and activation chunk is fetched once per 256 x 256 tile and shared by
-// the workgroup's waves (LLaDA-8B at 512 rows: gate/up 201 against 276 us, down 107
+// bf16 and int8 GEMMs over 256 or more token rows (prompts, wide windows) except the
+// LM head run the LDS-tiled kernel when it gives the chip at least TILED_MIN_WG
+// workgroups: every weight and activation chunk is fetched once per 256-row x 256-token
+// tile (int8: 128 tokens) and shared by the workgroup's waves (LLaDA-8B bf16 at 512
+// rows: gate/up 201 against 276 us, down 107
 // against 173; at 4096 rows gate/up 1063 against 2825, QKV 823 against 1735).  With
 // fewer workgroups the streaming layouts win (QKV at 512 rows, 96 tiles: 238
 // against 201 us; every GEMM of a 256-row window).  Models below the streaming
 // layouts' thresholds (test sizes) take it whenever it applies: it accepts any row
 // and token tile counts (ragged tiles are clamped).  The residual projections split
 // K until the chip holds ~256 workgroups (O/down at 512 rows: 32 tiles x 8 slices);
-// their partial buffer holds min(8 x rows, 4096) rows.
+// their partial buffer holds min(8 x rows, 4096) rows.  int8 weights take it for QKV
+// only: every wave widens the int8 chunks it reads from LDS, four times over per
+// chunk, which makes the larger projections VALU-bound (4096 rows: QKV 1460 -> 1118
+// us, but gate/up 1799 -> 1984 and down 855 -> 1086 against the whole-K layout).
 constexpr int TILED_MIN_WG = 192;
-bool tiled_layout(GemmKind k, int wt, int Mc) { return wt == WT_BF16 && k != G_LM && Mc >= 256; }
-int tiled_ks(GemmKind k, int n_tiles, int Mc) {
+bool tiled_layout(GemmKind k, int wt, int Mc) {
+    return Mc >= 256 && ((wt == WT_BF16 && k != G_LM) || (wt == WT_I8 && k == G_QKV));
+}
+// token tiles per workgroup of the tiled kernel
+int tiled_tt(int wt) { return wt == WT_I8 ? TiledShape<WT_I8>::TT : TiledShape<WT_BF16>::TT; }
+int tiled_ks(GemmKind k, int wt, int n_tiles, int Mc) {
     if (k != G_RES) return 1;
-    const long wgs = (long)ceil_div(n_tiles, TiledShape::RT) * ceil_div(Mc / 16, TiledShape::TT);
+    const long wgs = (long)ceil_div(n_tiles, 16) * ceil_div(Mc / 16, tiled_tt(wt));
     int ks = 1;
     while (ks < 8 && wgs * ks * 2 <= N_CU && (long)ks * 2 * Mc <= 4096) ks *= 2;
     return ks;
@@ -217,9 +225,9 @@ int template_nwn(GemmKind k) { return k == G_LM ? 4 : 1; }
 Decomp decomp(GemmKind k, int wt, int n_tiles, int Mc, int gy) {
     const int min_tiles = (k == G_QKV || k == G_RES) ? 128 : (k == G_GU ? 256 : 512);
     if (tiled_layout(k, wt, Mc)) {
-        const int ks = tiled_ks(k, n_tiles, Mc);
-        const long wgs = (long)ceil_div(n_tiles, TiledShape::RT) * ceil_div(Mc / 16, TiledShape::TT) * ks;
-        if (n_tiles < min_tiles || wgs >= TILED_MIN_WG) return Decomp{false, TiledShape::RT, ks, false, true};
+        const int ks = tiled_ks(k, wt, n_tiles, Mc);
+        const long wgs = (long)ceil_div(n_tiles, 16) * ceil_div(Mc / 16, tiled_tt(wt)) * ks;
+        if (n_tiles < min_tiles || wgs >= TILED_MIN_WG) return Decomp{false, 16, ks, false, true};
     }
     if (n_tiles < min_tiles) return Decomp{true, 1, 1};
     if (wide_layout(k, wt, gy)) return Decomp{false, WIDE_TILES, 1, true};
@@ -272,12 +280,13 @@ template <int WT, GemmKind KIND, class Epi>
 int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const Epi& epi, int gy, hipStream_t s) {
     GemmArgs g = g0;
     g.tpg = dc.tpg;
-    if constexpr (WT == WT_BF16 && KIND != G_LM) {
+    if constexpr ((WT == WT_BF16 && KIND != G_LM) || (WT == WT_I8 && KIND == G_QKV)) {
         if (dc.tiled) {
+            using TS = TiledShape<WT>;
             const int Mc = gy * MT * 16;
             if (Mc % 64 != 0) return fail(DLLM_E_INVAL, "internal: tiled GEMM needs 64-row blocks");
-            dim3 grid(ceil_div(n_tiles, TiledShape::RT), dc.ks, ceil_div(Mc / 16, TiledShape::TT));
-            hipLaunchKernelGGL((gemm_tiled_kernel<Epi>), grid, dim3(512), 0, s, g0, epi, Mc / 16);
+            dim3 grid(ceil_div(n_tiles, TS::RT), dc.ks, ceil_div(Mc / 16, TS::TT));
+            hipLaunchKernelGGL((gemm_tiled_kernel<WT, Epi>), grid, dim3(512), 0, s, g0, epi, Mc / 16);
             return DLLM_OK;
         }
     }

@@ -1,17 +1,18 @@
-// Tiled GEMM for many token rows (prompt processing): Y = X W^T with bf16 weights,
-// where the streaming kernel's waves each fetch their own operand fragments and the
-// matrix cores stay ~30% busy.
+// Tiled GEMM for many token rows (prompt processing): Y = X W^T with bf16 or int8
+// weights, where the streaming kernel's waves each fetch their own operand fragments
+// and the matrix cores stay ~30% busy.
 //
-// Workgroup = 8 waves = 2 row halves x 4 token quarters; it owns 16 row tiles x 16
-// token tiles (256 rows x 256 tokens) and a K range (split-K over grid.y, for the
-// residual projections' partial sums).  Each K step (one 32-column chunk) its 16
-// weight chunks and 16 x 2 activation chunks (hi, lo planes) are copied once into
-// LDS with direct global->LDS loads, three stages deep, and every wave multiplies
-// its 8 row tiles by its 4 token tiles from there: 64 MFMAs per 16 KiB of LDS reads,
-// against 16 KiB of L1/L2 fetches per 64 MFMAs in the streaming layouts.  The
-// packed formats are the streaming kernel's (chunks are already in MFMA fragment
-// order, so an LDS chunk is read with one 16-byte load per lane).  Results go
-// through the same epilogues, in four passes of 64 tokens.
+// Workgroup = 8 waves = 2 row halves x 4 token quarters; it owns 16 row tiles x TT
+// token tiles (bf16: 256 rows x 256 tokens; int8: 256 x 128) and a K range (split-K
+// over grid.y, for the residual projections' partial sums).  Each K step (one weight
+// chunk: 32 columns bf16, 64 int8) its 16 weight chunks and the token tiles'
+// activation chunks (hi, lo planes; two per token tile for int8) are copied once into
+// LDS with direct global->LDS loads, three stages deep, and every wave multiplies its
+// 8 row tiles by its token tiles from there: 64 MFMAs per 16 KiB of LDS reads, against
+// 16 KiB of L1/L2 fetches per 64 MFMAs in the streaming layouts.  The packed formats
+// are the streaming kernel's (chunks are already in MFMA fragment order, so an LDS
+// chunk is read with one 16-byte load per lane; int8 is widened to bf16 after the
+// read).  Results go through the same epilogues, in four passes of TT / 4 token tiles.
 #pragma once
 
 #include "gemm.hpp"
@@ -20,23 +21,29 @@ namespace dllm {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+template <int WT>
 struct TiledShape {
-    static constexpr int RT = 16, TT = 16;   // row tiles, token tiles per workgroup
-    static constexpr int WR = 8, WM = 4;     // per wave
-    static constexpr int S = 3;              // LDS stages
-    static constexpr int WB = RT * 1024;     // weight bytes per stage
-    static constexpr int XB = TT * 2048;     // activation bytes per stage (hi + lo)
+    static_assert(WT == WT_BF16 || WT == WT_I8, "tiled GEMM: bf16 or int8 weights");
+    static constexpr int XPER = WTraits<WT>::XPER;   // activation chunks per weight chunk
+    static constexpr int RT = 16;                    // row tiles per workgroup
+    static constexpr int WM = 4 / XPER;              // token tiles per wave
+    static constexpr int TT = 4 * WM;                // token tiles per workgroup
+    static constexpr int WR = 8;                     // row tiles per wave
+    static constexpr int S = 3;                      // LDS stages
+    static constexpr int WB = RT * 1024;             // weight bytes per stage
+    static constexpr int XB = TT * XPER * 2048;      // activation bytes per stage (hi + lo)
     static constexpr int SB = WB + XB;
-    static constexpr int LOADS = (RT + 2 * TT) / 8;   // 1 KiB global->LDS loads per wave and stage
+    static constexpr int LOADS = (RT + 2 * XPER * TT) / 8;   // 1 KiB global->LDS loads per wave and stage
     static constexpr int LDY = 16 * WM + 1;
 };
 
 // m_tiles: token tiles of X (its rows / 16, a multiple of 4); rows past them are
 // never read (loads clamp to the last tile) and never written.
-template <class Epi>
+template <int WT, class Epi>
 __global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, int m_tiles) {
-    using T = TiledShape;
-    static_assert(T::LOADS * 8 == T::RT + 2 * T::TT, "stage loads must split evenly over the waves");
+    using T = TiledShape<WT>;
+    constexpr int XPER = T::XPER;
+    static_assert(T::LOADS * 8 == T::RT + 2 * XPER * T::TT, "stage loads must split evenly over the waves");
     static_assert(16 * T::RT * T::LDY * 4 <= T::S * T::SB, "epilogue tile must fit the stage buffers");
     __shared__ __attribute__((aligned(1024))) char sm[T::S * T::SB];
     constexpr int ESM = Epi::kSmem > 0 ? Epi::kSmem : 16;
@@ -49,8 +56,9 @@ __global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, in
     const unsigned KS = gridDim.y;
     const int c0 = (int)((blockIdx.y * (unsigned)KC) / KS), c1 = (int)(((blockIdx.y + 1) * (unsigned)KC) / KS);
 
-    // stage slot i: i < RT the weight chunk of row tile nt0 + i, else the activation
-    // chunk (token tile (i - RT) / 2, plane (i - RT) % 2); wave w copies slots w + 8j
+    // stage slot i: i < RT the weight chunk of row tile nt0 + i, else activation chunk
+    // q = i - RT: token tile q / (2 XPER), column half (q / 2) % XPER, plane q % 2;
+    // wave w copies slots w + 8j
     auto stage = [&](int c, int buf) {
         char* base = sm + buf * T::SB;
 #pragma unroll
@@ -63,10 +71,10 @@ __global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, in
                 src = (const char*)g.W + (((size_t)nt * KC + c) * 64 + lane) * 16;
                 dst = base + i * 1024;
             } else {
-                const int q = i - T::RT, tt = q >> 1, pl = q & 1;
+                const int q = i - T::RT, tt = q / (2 * XPER), h = (q >> 1) % XPER, pl = q & 1;
                 const int mt = min(mt0 + tt, m_tiles - 1);
-                src = (const char*)g.X + ((size_t)mt * g.KCx + c) * 2048 + pl * 1024 + lane * 16;
-                dst = base + T::WB + tt * 2048 + pl * 1024;
+                src = (const char*)g.X + ((size_t)mt * g.KCx + c * XPER + h) * 2048 + pl * 1024 + lane * 16;
+                dst = base + T::WB + q * 1024;
             }
             __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)dst, 16, 0, 0);
         }
@@ -95,27 +103,39 @@ __global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, in
             stage(min(c + 2, c1 - 1), (c - c0 + 2) % T::S);
             const char* Wb = sm + cur * T::SB;
             const char* Xb = Wb + T::WB;
-            u32x4_t xh[T::WM], xl[T::WM];
+            u32x4_t xh[T::WM][XPER], xl[T::WM][XPER];
 #pragma unroll
-            for (int t = 0; t < T::WM; ++t) {
-                xh[t] = *(const u32x4_t*)(Xb + (T::WM * wq + t) * 2048 + lane * 16);
-                xl[t] = *(const u32x4_t*)(Xb + (T::WM * wq + t) * 2048 + 1024 + lane * 16);
-            }
+            for (int t = 0; t < T::WM; ++t)
+#pragma unroll
+                for (int h = 0; h < XPER; ++h) {
+                    const char* xp = Xb + (((T::WM * wq + t) * XPER + h) * 2) * 1024 + lane * 16;
+                    xh[t][h] = *(const u32x4_t*)xp;
+                    xl[t][h] = *(const u32x4_t*)(xp + 1024);
+                }
 #pragma unroll
             for (int f = 0; f < T::WR; ++f) {
-                const u32x4_t w = *(const u32x4_t*)(Wb + (T::WR * wr + f) * 1024 + lane * 16);
-#pragma unroll
-                for (int t = 0; t < T::WM; ++t) {
-                    acc[f][t] = mfma_bf16(w, xh[t], acc[f][t]);
-                    acc[f][t] = mfma_bf16(w, xl[t], acc[f][t]);
+                const u32x4_t raw = *(const u32x4_t*)(Wb + (T::WR * wr + f) * 1024 + lane * 16);
+                u32x4_t w[XPER];
+                if constexpr (WT == WT_I8) {
+                    w[0] = i8x8_to_bf16x8(raw[0], raw[1]);
+                    w[XPER - 1] = i8x8_to_bf16x8(raw[2], raw[3]);
+                } else {
+                    w[0] = raw;
                 }
+#pragma unroll
+                for (int h = 0; h < XPER; ++h)
+#pragma unroll
+                    for (int t = 0; t < T::WM; ++t) {
+                        acc[f][t] = mfma_bf16(w[h], xh[t][h], acc[f][t]);
+                        acc[f][t] = mfma_bf16(w[h], xl[t][h], acc[f][t]);
+                    }
             }
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
     __syncthreads();
 
-    // epilogue: four passes of 64 tokens over the stage buffers (rows 0..255 of Y)
+    // epilogue: four passes of WM token tiles over the stage buffers (rows 0..255 of Y)
     float* Y = (float*)sm;
     const int nrows = 16 * max(0, min(T::RT, g.n_tiles - nt0));
     const int r = lane & 15, gq = lane >> 4;
