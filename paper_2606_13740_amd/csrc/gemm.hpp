@@ -341,7 +341,7 @@ gemm_kernel(GemmArgs g, Epi epi) {
         const int nf = max(0, min(g.tpg, g.n_tiles - nt0));
         if (nf == 0) break;
         if (g.wscale != nullptr || g.bias != nullptr) {
-            for (int idx = threadIdx.x; idx < NR * MR; idx += blockDim.x) {
+            for (int idx = threadIdx.x; idx < 16 * nf * MR; idx += blockDim.x) {
                 const int n = idx / MR, m = idx % MR;
                 float y = Y[q][n * LDY + m];
                 if (g.wscale != nullptr) y *= g.wscale[nt0 * 16 + n];
