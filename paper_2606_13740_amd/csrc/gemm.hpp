@@ -314,6 +314,15 @@ gemm_kernel(GemmArgs g, Epi epi) {
                             loadx(sx, c + DX);
                         }
                     }
+                    // a last round whose chunks are all loaded: computes only (QKV, O
+                    // and down at the LLaDA-8B widths end this way; gate/up's 16 chunks
+                    // per wave over 3 stages leave 4, which take the conditional steps)
+                    if (c1 - base <= D) {
+#pragma unroll
+                        for (int s = 0; s < D; ++s)
+                            if (base + s < c1) compute(s, s % DX);
+                        base = c1;
+                    }
                 }
             }
             for (; base < c1; base += D) {
