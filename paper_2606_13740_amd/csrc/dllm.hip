@@ -166,6 +166,11 @@ struct Decomp {
 };
 
 constexpr int N_CU = 256;
+// A second gate/up template for widths that fill the chip in one round only with more
+// than 6 row tiles per wave group (Dream-7B: 2368 row tiles, 10 per group in 237
+// workgroups: 46.2 against 53.1 us for 5 per group in two rounds).  It runs 2 weight
+// stages where the 6-tile template runs 3, so the LLaDA-8B widths keep the 6-tile one.
+constexpr int GU_WIDE_TILES = 10;
 
 // bf16 and int8 GEMMs over 256 or more token rows (prompts, wide windows) except the
 // LM head run the LDS-tiled kernel when it gives the chip at least TILED_MIN_WG
@@ -234,7 +239,11 @@ Decomp decomp(GemmKind k, int wt, int n_tiles, int Mc, int gy) {
     const int fw = template_fw(k, wt, Mc / (16 * gy)), nwn = template_nwn(k);
     Decomp best{false, 1, 1};
     double best_load = 1e30;
-    for (int tpg = fw; tpg >= 1; --tpg) {
+    // bf16 gate/up up to 2 token tiles may also take the 10-tile template
+    // (GU_WIDE_TILES), for widths whose row tiles would need two rounds at 6
+    const int mt = Mc / (16 * gy);
+    const int fw_max = (k == G_GU && wt == WT_BF16 && mt <= 2) ? GU_WIDE_TILES : fw;
+    for (int tpg = fw_max; tpg >= 1; --tpg) {
         for (int ks = (k == G_RES && Mc <= 64) ? RES_SPLIT : 1; ks >= 1; ks >>= 1) {
             const long wgs = (long)ceil_div(ceil_div(n_tiles, tpg), nwn) * ks * gy;
             // busiest CU: rounds x (its tiles of full K + a workgroup's fixed cost, about
@@ -291,6 +300,14 @@ int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const
         }
     }
     if (dc.small) return launch_gemm_mt<WT, -1, 1, 4>(MT, g, epi, n_tiles, dc.ks, gy, s);
+    if constexpr (KIND == G_GU && WT == WT_BF16) {
+        if (g.tpg > template_fw(G_GU, WT, MT)) {
+            if (g.tpg > GU_WIDE_TILES || MT > 2) return fail(DLLM_E_INVAL, "internal: gate/up tiles outside the templates");
+            if (MT == 1) launch_gemm_inst<WT, GU_WIDE_TILES, 1, 8, 1>(g, epi, n_tiles, 1, gy, s);
+            else launch_gemm_inst<WT, GU_WIDE_TILES, 1, 8, 2>(g, epi, n_tiles, 1, gy, s);
+            return DLLM_OK;
+        }
+    }
     if constexpr ((WT == WT_BF16 || WT == WT_I8) && (KIND == G_GU || KIND == G_RES)) {
         if (dc.wide) {
             if (MT != 4 || g.tpg != WIDE_TILES) return fail(DLLM_E_INVAL, "internal: wide layout needs 64-row blocks");
