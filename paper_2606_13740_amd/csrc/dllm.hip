@@ -155,14 +155,15 @@ int pick_MT(int M) {
 // share, rounds x (tpg / ks + 1) row tiles of full K, the 1 standing for a
 // workgroup's fixed cost (start-up, K-slice reduction, epilogue); this picks the
 // layouts above at the LLaDA-8B widths (256 or 247 workgroups) and e.g. 5 tiles
-// per wave group for the Dream-7B gate/up and LM head.  Small models (fewer row
-// tiles than the thresholds below) use one tile per 4-wave workgroup.
+// per wave group for the Dream-7B LM head (its gate/up takes the 10-tile template
+// below).  Small models (fewer row tiles than the thresholds below) use one tile per
+// 4-wave workgroup.
 struct Decomp {
     bool small;   // 1 tile per workgroup of 4 waves, K over the waves
     int tpg;      // row tiles per wave group
     int ks;       // split-K slices (residual projections)
     bool wide = false;   // long prompts: whole-K waves of 8 row tiles (WIDE_TILES)
-    bool tiled = false;  // 256+ rows, bf16: gemm_tiled_kernel (LDS-staged 256 x 256 tiles)
+    bool tiled = false;  // 256+ rows: gemm_tiled_kernel (LDS-staged tiles; tiled_layout)
 };
 
 constexpr int N_CU = 256;
@@ -176,10 +177,10 @@ constexpr int GU_WIDE_TILES = 10;
 // LM head run the LDS-tiled kernel when it gives the chip at least TILED_MIN_WG
 // workgroups: every weight and activation chunk is fetched once per 256-row x 256-token
 // tile (int8: 128 tokens) and shared by the workgroup's waves (LLaDA-8B bf16 at 512
-// rows: gate/up 201 against 276 us, down 107
-// against 173; at 4096 rows gate/up 1063 against 2825, QKV 823 against 1735).  With
-// fewer workgroups the streaming layouts win (QKV at 512 rows, 96 tiles: 238
-// against 201 us; every GEMM of a 256-row window).  Models below the streaming
+// rows: gate/up 201 against 276 us, down 107 against 173; at 4096 rows gate/up 1063
+// against 2825, QKV 823 against 1735).  With fewer workgroups the streaming layouts
+// win (QKV at 512 rows, 96 tiles: 238 against 201 us; every GEMM of a 256-row
+// window).  Models below the streaming
 // layouts' thresholds (test sizes) take it whenever it applies: it accepts any row
 // and token tile counts (ragged tiles are clamped).  The residual projections split
 // K until the chip holds ~256 workgroups (O/down at 512 rows: 32 tiles x 8 slices);
@@ -214,7 +215,6 @@ constexpr int WIDE_TILES = 8;
 bool wide_layout(GemmKind k, int wt, int gy) {
     return gy > 8 && (k == G_GU || k == G_RES) && (wt == WT_BF16 || wt == WT_I8);
 }
-
 
 // Row tiles per wave group of each template at mt token tiles.  Q4_0 exceptions:
 // the LM head takes 4, since at 8 its code pipeline, activations and 16
