@@ -307,7 +307,7 @@ def run_e2e_mbsd(args, dl, torch, shape, dev):
                     lookahead_steps=sum(1 for e in tr if e["R"] > WN), rows_total=sum(e["W"] for e in tr))
 
     runs = {}
-    # (acceptance threshold, lookahead allowance); the last run allows the +12% of a
+    # (acceptance threshold, lookahead allowance); the last run allows the +12-14% of a
     # 48-row window, so the window grows at the end of every block
     for theta, allowance in ((0.9, 0.1), (0.0, 0.1), (0.0, 0.15)):
         generate(theta, allowance)               # warmup (untimed)
