@@ -377,6 +377,19 @@ int dllm_record_drafts(const int32_t* d_id, const uint8_t* d_mask, int32_t* d_dr
 int dllm_quantize_q4_0(const void* d_src, int32_t src_dtype, int32_t rows, int32_t K, uint8_t* d_codes,
                        uint16_t* d_scales, dllm_stream stream);
 
+/* int8 quantisation, the converter step for DLLM_W8 models (Implementation: the
+ * model converter packs quantised weights; the per-output-row int8 form is the
+ * analog of the paper's Q4_0): for every row of the row-major [rows][K] source
+ * (float for src_dtype DLLM_F32, bfloat16 for DLLM_BF16; device), in fp32:
+ * s = max|w| / 127 and q = round-half-even(w / s) clamped to [-127, 127], both
+ * divisions correctly rounded (a zero row gets s = 0 and codes 0); the weight q
+ * stands for is q * s.  This is the quantiser dllm_model_create applies to DLLM_W8
+ * models.  Writes d_codes [rows][K] and d_scales [rows] (caller-owned device
+ * buffers) asynchronously on `stream`.  E_INVAL for NULL pointers or rows, K < 1;
+ * E_DTYPE for another src_dtype. */
+int dllm_quantize_int8(const void* d_src, int32_t src_dtype, int32_t rows, int32_t K, int8_t* d_codes,
+                       float* d_scales, dllm_stream stream);
+
 /* Measurement helper: one launch of a plain streaming read over `bytes` bytes of
  * the device buffer d_buf (16-byte aligned; bytes a multiple of 16), the same
  * 16-byte-per-lane non-temporal loads the GEMMs stream weights with.  The caller

@@ -91,17 +91,25 @@ def group_heads(KV: np.ndarray, n_heads: int) -> np.ndarray:
 
 def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray, limits: np.ndarray) -> np.ndarray:
     """Row i (all heads) attends to keys [0, limits[i]) of K, V [keys, Hkv, Dh]
-    (query head h uses K/V head h // (H / Hkv))."""
+    (query head h uses K/V head h // (H / Hkv)).
+
+    Rows that share a key limit are evaluated together, a few hundred at a time,
+    as per-head matrix products (scores [H, rows, keys], softmax over keys, then
+    the weighted sum of V): the same formula as one row at a time."""
     n, H, dh = q.shape
     out = np.zeros_like(q)
     scale = 1.0 / np.sqrt(dh)
-    for i in range(n):
-        lim = int(limits[i])
-        k = group_heads(K[:lim], H)                         # [lim, H, Dh]
-        v = group_heads(V[:lim], H)
-        s = np.einsum("hd,khd->hk", q[i], k) * scale        # [H, lim]
-        p = softmax(s)
-        out[i] = np.einsum("hk,khd->hd", p, v)
+    limits = np.asarray(limits)
+    for lim in np.unique(limits):
+        lim = int(lim)
+        rows = np.flatnonzero(limits == lim)
+        k = group_heads(K[:lim], H).transpose(1, 2, 0)      # [H, Dh, lim]
+        v = group_heads(V[:lim], H).transpose(1, 0, 2)      # [H, lim, Dh]
+        for c0 in range(0, len(rows), 256):
+            r = rows[c0:c0 + 256]
+            s = np.matmul(q[r].transpose(1, 0, 2), k) * scale   # [H, rows, lim]
+            p = softmax(s)
+            out[r] = np.matmul(p, v).transpose(1, 0, 2)         # [rows, H, Dh]
     return out
 
 
@@ -497,9 +505,14 @@ def commit_staged(conf: np.ndarray, pred: np.ndarray, tok: np.ndarray, mask: np.
       it takes its predicted id and leaves the mask.
     - If none did and invisible positions remain, the most confident of them becomes
       visible (equal confidence -> lower position), so that decoding always progresses.
-    - Every visible position, the ones just promoted included, whose confidence reaches
-      theta_stable becomes stable.  A visible position keeps its id here: identity
-      revision of visible tokens goes through the refresh path.
+    - Every visible position, the ones just promoted included, whose held token passes
+      the stability criterion becomes stable: this step predicts the id the position
+      holds (pred == tok) with a confidence that reaches theta_stable.  Stability is a
+      property of the held token; a row whose prediction moved to another id, however
+      confidently, stays visible and tracked.  For theta_stable > 1/2 this is exactly
+      "the held token's own probability reaches theta_stable", since a token other
+      than the argmax has probability at most 1 - conf < 1/2.  A visible position keeps
+      its id here: identity revision of visible tokens goes through the refresh path.
 
     Confidences and thresholds are compared in float32 (the precision the confidence
     is produced in).  Returns the positions that left the invisible state, ascending.
@@ -516,9 +529,56 @@ def commit_staged(conf: np.ndarray, pred: np.ndarray, tok: np.ndarray, mask: np.
         mask[p] = 0
         state[p] = V
     for p in seg:
-        if state[p] == V and c[p] >= ts:
+        if state[p] == V and c[p] >= ts and pred[p] == tok[p]:
             state[p] = S
     return np.array(sorted(promoted), dtype=np.int32)
+
+
+def repredict_tracked(model: OracleModel, kv: OracleKV, tracked: dict, theta_visible: float,
+                      theta_stable: float):
+    """Re-prediction of the visible tokens that stay tracked after their block entered
+    the prefix (System Design, "Staged Token Stabilization": visible tokens remain
+    tracked until they pass the stability threshold; "Sparse Cache Refresh": their
+    confidence, identity and KV are recomputed sparsely and merged before the next
+    step).
+
+    `tracked` maps a prefix position to the id it holds.  The tracked positions are
+    taken block by block, in block order.  For block b:
+      1. every tracked position of b is recomputed at once as MASK (one sparse refresh:
+         their K/V replace the cached ones layer by layer, each row attends to the keys
+         up to the end of its block), which gives the model's (id, conf) for it with
+         the block's other tracked tokens hidden and everything else as it stands;
+      2. per position, in float32: conf >= theta_stable -> the new id, and the position
+         becomes stable (no longer tracked); conf >= theta_visible -> the new id, still
+         visible; otherwise it keeps its id;
+      3. the chosen ids of block b are written back with a second sparse refresh, so
+         the cache holds their K/V before block b + 1 is re-predicted.
+    The result depends only on the tracked set and the cache, not on how many rows
+    one call may carry.  Updates `tracked` in place; returns (positions that became
+    stable, ascending; {position: id written back})."""
+    tv, ts = np.float32(theta_visible), np.float32(theta_stable)
+    mask_id = model.shape.mask_id
+    stable, chosen = [], {}
+    for b in sorted({kv.block_of(int(p)) for p in tracked}):
+        pos = sorted(int(p) for p in tracked if kv.block_of(int(p)) == b)
+        ids, conf, _ = refresh(model, kv, pos, [mask_id] * len(pos))
+        new = []
+        for j, p in enumerate(pos):
+            c = np.float32(conf[j])
+            if c >= ts:
+                new.append(int(ids[j]))
+                stable.append(p)
+            elif c >= tv:
+                new.append(int(ids[j]))
+            else:
+                new.append(int(tracked[p]))
+        refresh(model, kv, pos, new, lm_head=False)
+        for p, t in zip(pos, new):
+            chosen[p] = t
+            tracked[p] = t
+    for p in stable:
+        del tracked[p]
+    return sorted(stable), chosen
 
 
 def commit_schedule(n_masked: int, steps: int) -> list:

@@ -78,6 +78,7 @@ _SIGNATURES = {
     "dllm_kernel_replay": ([_vp, _vp, _i32, _i32, _i32, _vp], ctypes.c_int),
     "dllm_read_bandwidth": ([_vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
     "dllm_quantize_q4_0": ([_vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_quantize_int8": ([_vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_commit_staged": ([_vp, _vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_float, ctypes.c_float, _vp, _vp, _vp],
                            ctypes.c_int),
 }
@@ -258,6 +259,11 @@ def dllm_quantize_q4_0(src, src_dtype: int, rows: int, K: int, codes, scales, st
            "dllm_quantize_q4_0")
 
 
+def dllm_quantize_int8(src, src_dtype: int, rows: int, K: int, codes, scales, stream=None):
+    _check(lib().dllm_quantize_int8(_ptr(src), src_dtype, rows, K, _ptr(codes), _ptr(scales), _stream(stream)),
+           "dllm_quantize_int8")
+
+
 def dllm_read_bandwidth(buf, nbytes: int, sink, stream=None):
     _check(lib().dllm_read_bandwidth(_ptr(buf), nbytes, _ptr(sink), _stream(stream)), "dllm_read_bandwidth")
 
@@ -371,6 +377,10 @@ class KVCache:
     @property
     def prefix_len(self) -> int:
         return dllm_kv_prefix_len(self.handle)[0]
+
+    @property
+    def prompt_len(self) -> int:
+        return dllm_kv_prefix_len(self.handle)[1]
 
     def close(self):
         if getattr(self, "handle", None):

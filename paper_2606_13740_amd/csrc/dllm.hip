@@ -1179,6 +1179,21 @@ int dllm_quantize_q4_0(const void* d_src, int32_t src_dtype, int32_t rows, int32
     return DLLM_OK;
 }
 
+int dllm_quantize_int8(const void* d_src, int32_t src_dtype, int32_t rows, int32_t K, int8_t* d_codes,
+                       float* d_scales, dllm_stream stream) {
+    if (!d_src || !d_codes || !d_scales) return fail(DLLM_E_INVAL, "NULL argument");
+    if (rows < 1 || K < 1) return fail(DLLM_E_INVAL, "rows and K must be >= 1");
+    if (src_dtype != DLLM_F32 && src_dtype != DLLM_BF16) return fail(DLLM_E_DTYPE, "source must be DLLM_F32 or DLLM_BF16");
+    if (src_dtype == DLLM_F32)
+        hipLaunchKernelGGL((quantize_i8_kernel<float>), dim3(rows), dim3(256), 0, (hipStream_t)stream,
+                           (const float*)d_src, K, d_codes, d_scales);
+    else
+        hipLaunchKernelGGL((quantize_i8_kernel<uint16_t>), dim3(rows), dim3(256), 0, (hipStream_t)stream,
+                           (const uint16_t*)d_src, K, d_codes, d_scales);
+    HIP_TRY(hipGetLastError());
+    return DLLM_OK;
+}
+
 int dllm_read_bandwidth(const void* d_buf, size_t bytes, uint32_t* d_sink, dllm_stream stream) {
     if (!d_buf || !d_sink) return fail(DLLM_E_INVAL, "NULL argument");
     if (((uintptr_t)d_buf & 15) != 0 || (bytes & 15) != 0)

@@ -250,9 +250,10 @@ commit_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, int seg
 // Staged token stabilisation over one segment (one thread per position, <= 1024):
 // state 0 invisible (masked), 1 visible, 2 stable.  Invisible positions at or
 // above tv become visible (taking their predicted id); if there is none, the
-// most confident invisible position does (ties: lower position); visible
-// positions at or above ts become stable.  The promoted positions are written
-// in ascending order.
+// most confident invisible position does (ties: lower position); a visible
+// position becomes stable when this step predicts the id it holds with a
+// confidence at or above ts (stability is a property of the held token).  The
+// promoted positions are written in ascending order.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(1024)
 commit_staged_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, uint8_t* state, int seg_begin,
@@ -264,6 +265,8 @@ commit_staged_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, 
     const int p = seg_begin + i;
     const uint8_t st = in ? state[p] : (uint8_t)2;
     const float c = in ? conf[p] : 0.f;
+    const int pid = in ? id[p] : 0;
+    const int held = in ? tok[p] : 0;
     const bool cand = in && st == 0;
     if (i == 0) best = 0ull;
     const bool vis = cand && c >= tv;
@@ -277,10 +280,10 @@ commit_staged_kernel(const float* conf, const int* id, int* tok, uint8_t* mask, 
         prom = cand && best != 0ull && (int)(1024u - (unsigned)(best & 0xFFFFFFFFull)) == i;
     }
     uint8_t ns = prom ? (uint8_t)1 : st;
-    if (ns == 1 && c >= ts) ns = 2;
+    if (ns == 1 && c >= ts && (prom || pid == held)) ns = 2;
     if (in) {
         if (prom) {
-            tok[p] = id[p];
+            tok[p] = pid;
             mask[p] = 0;
         }
         if (ns != st) state[p] = ns;
@@ -337,6 +340,16 @@ __global__ void __launch_bounds__(256) pack_bias_kernel(PackSrc p, int n_rows_pa
     out[r] = src ? src[row] : 0.f;
 }
 
+// int8 quantiser (per output row, decided in fp32): s = max|w| / 127 and
+// q = round-half-even(w / s) clamped to [-127, 127], both divisions correctly
+// rounded; a zero row has s = 0 and all codes 0.
+__device__ __forceinline__ float i8_scale(float amax) { return __fdiv_rn(amax, 127.0f); }
+__device__ __forceinline__ int i8_code(float x, float s) {
+    if (!(s > 0.f)) return 0;
+    const int q = (int)rintf(__fdiv_rn(x, s));
+    return max(-127, min(127, q));
+}
+
 // One thread per 16-byte lane slot.  ST: source element type (float / uint16_t bf16).
 template <int WT, typename ST>
 __global__ void __launch_bounds__(256)
@@ -377,11 +390,7 @@ pack_kernel(PackSrc p, int n_tiles, int KCw, u32x4_t* out, const float* scale) {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const int k = kc * 64 + 32 * hh + 8 * g + e;
-                    int qv = 0;
-                    if (k < p.K && sc > 0.f) {
-                        qv = (int)rintf(__fdiv_rn(to_f32<ST>(s[k]), sc));
-                        qv = max(-127, min(127, qv));
-                    }
+                    const int qv = (k < p.K) ? i8_code(to_f32<ST>(s[k]), sc) : 0;
                     b[8 * hh + e] = (uint32_t)(qv & 0xFF);
                 }
 #pragma unroll
@@ -470,7 +479,30 @@ __global__ void __launch_bounds__(256) row_scale_kernel(PackSrc p, int n_rows_pa
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
     __syncthreads();
     if (threadIdx.x == 0 && r < n_rows_padded)
-        scale[r] = __fdiv_rn(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])), 127.0f);
+        scale[r] = i8_scale(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+}
+
+// int8 quantisation to plain row-major arrays (the converter's output, and the form
+// the quantiser is checked in): one workgroup per row; codes [rows][K], scales [rows].
+template <typename ST>
+__global__ void __launch_bounds__(256)
+quantize_i8_kernel(const ST* w, int K, int8_t* codes, float* scales) {
+    __shared__ float red[4];
+    __shared__ float s_sh;
+    const int r = blockIdx.x;
+    const ST* row = w + (size_t)r * K;
+    float mx = 0.f;
+    for (int k = threadIdx.x; k < K; k += blockDim.x) mx = fmaxf(mx, fabsf(to_f32<ST>(row[k])));
+    mx = warp_max(mx);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        s_sh = i8_scale(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+        scales[r] = s_sh;
+    }
+    __syncthreads();
+    const float sc = s_sh;
+    for (int k = threadIdx.x; k < K; k += blockDim.x) codes[(size_t)r * K + k] = (int8_t)i8_code(to_f32<ST>(row[k]), sc);
 }
 
 // (cos, sin) of pos * base^(-2j/Dh), evaluated in double.

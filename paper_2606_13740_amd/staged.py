@@ -11,13 +11,19 @@ the tracked set (the Implementation section gives token-state transitions and
 refresh candidates to the host runtime); every arithmetic step runs in the
 library.
 
-Re-prediction of a tracked position (a reading of the Sparse Cache Refresh
-passage, which recomputes confidence, identity and KV): the position is
-refreshed with the MASK id, which yields the model's (id, conf) for it in the
-current context; it becomes stable with that id if conf >= theta_stable, takes
-that id but stays visible if conf >= theta_visible, and keeps its id otherwise;
-then the chosen ids are written back with a second refresh, so the cache holds
-their K/V.
+Re-prediction of the tracked positions (a reading of the Staged Token
+Stabilization and Sparse Cache Refresh passages: confidence, identity and KV of
+tracked visible tokens are recomputed sparsely until they pass the stability
+threshold), block by block in block order: all tracked positions of a block are
+refreshed at once with the MASK id, which yields the model's (id, conf) for each
+in the current context; conf >= theta_stable -> that id and the position becomes
+stable (no longer tracked), conf >= theta_visible -> that id, still visible,
+otherwise it keeps its id; the chosen ids are written back with a second refresh
+before the next block is re-predicted.  The decisions therefore depend only on the
+tracked set and the cache, not on how many rows one call may carry.  A block's
+write-back and the next block's re-prediction share one refresh call when they fit
+(a row of block b attends only up to the end of block b, so it is unaffected by
+the next block's rows in the same call).
 """
 import numpy as np
 import torch
@@ -35,6 +41,8 @@ class StagedGenerator:
         sh = model.shape
         self.B, self.mask_id = sh.block, sh.mask_id
         self.max_rows = model.cfg.max_window
+        if self.max_rows < self.B:
+            raise ValueError("staged generation needs max_window >= the block size")
         self.tracked = {}             # prefix position -> current id of a visible token
         self.steps = []               # denoising steps per block
         self.promoted = []            # positions promoted per step (host copies, for inspection)
@@ -71,37 +79,50 @@ class StagedGenerator:
         return t, st
 
     def refresh_visible(self):
-        """Re-predict every tracked visible position of the prefix (in chunks of at most
-        max_window rows, each chunk one re-prediction refresh and one write-back).
-        Returns (positions that became stable, {position: id written back})."""
+        """Re-predict every tracked visible position of the prefix, block by block.
+        Returns (positions that became stable, ascending; {position: id written back})."""
+        P0, B, mask_id, dev = self.kv.prompt_len, self.B, self.mask_id, self.dev
+        h, kvh = self.model.handle, self.kv.handle
+        by_block = {}
+        for p in sorted(self.tracked):
+            by_block.setdefault((p - P0) // B, []).append(p)
         became_stable, chosen = [], {}
-        pos_all = sorted(self.tracked)
-        for c0 in range(0, len(pos_all), self.max_rows):
-            pos = np.array(pos_all[c0:c0 + self.max_rows], dtype=np.int32)
+        wb_pos, wb_ids = [], []          # the previous block's write-back, not issued yet
+
+        def refresh(pos, ids, want_out):
             n = len(pos)
-            d_pos = torch.from_numpy(pos).to(self.dev)
-            rid = torch.empty(n, dtype=torch.int32, device=self.dev)
-            rconf = torch.empty(n, device=self.dev)
-            masked = torch.full((n,), self.mask_id, dtype=torch.int32, device=self.dev)
-            dllm_refresh_kv(self.model.handle, self.kv.handle, d_pos, masked, n, rid, rconf, self.stream)
-            ids, conf = rid.cpu().numpy(), rconf.cpu().numpy()
-            new = np.empty(n, dtype=np.int32)
+            d_pos = torch.tensor(pos, dtype=torch.int32, device=dev)
+            d_ids = torch.tensor(ids, dtype=torch.int32, device=dev)
+            rid = torch.empty(n, dtype=torch.int32, device=dev) if want_out else None
+            rconf = torch.empty(n, device=dev) if want_out else None
+            dllm_refresh_kv(h, kvh, d_pos, d_ids, n, rid, rconf, self.stream)
+            return rid, rconf
+
+        for b in sorted(by_block):
+            pos = by_block[b]
+            if len(wb_pos) + len(pos) > self.max_rows and wb_pos:
+                refresh(wb_pos, wb_ids, False)
+                wb_pos, wb_ids = [], []
+            rid, rconf = refresh(wb_pos + pos, wb_ids + [mask_id] * len(pos), True)
+            self._sync()
+            ids = rid.cpu().numpy()[len(wb_pos):]
+            conf = rconf.cpu().numpy()[len(wb_pos):]
+            new = []
             for j, p in enumerate(pos):
-                p = int(p)
-                if conf[j] >= np.float32(self.ts):
-                    new[j] = ids[j]
+                c = np.float32(conf[j])
+                if c >= np.float32(self.ts):
+                    new.append(int(ids[j]))
                     became_stable.append(p)
-                elif conf[j] >= np.float32(self.tv):
-                    new[j] = ids[j]
+                elif c >= np.float32(self.tv):
+                    new.append(int(ids[j]))
                 else:
-                    new[j] = self.tracked[p]
-            dllm_refresh_kv(self.model.handle, self.kv.handle, d_pos, torch.from_numpy(new).to(self.dev), n,
-                            None, None, self.stream)
-            for j, p in enumerate(pos):
-                self.tracked[int(p)] = int(new[j])
-                chosen[int(p)] = int(new[j])
+                    new.append(self.tracked[p])
+            for p, t in zip(pos, new):
+                self.tracked[p] = t
+                chosen[p] = t
+            wb_pos, wb_ids = pos, new
+        if wb_pos:
+            refresh(wb_pos, wb_ids, False)
         for p in became_stable:
             del self.tracked[p]
-        return became_stable, chosen
-
-
+        return sorted(became_stable), chosen

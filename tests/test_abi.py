@@ -147,3 +147,13 @@ def test_commit_staged_validates_on_host(dl, args, code):
 
 def test_version_string(dl):
     assert dl.lib().dllm_version().startswith(b"dllm")
+
+
+def test_quantizers_validate_on_host(dl):
+    L = dl.lib()
+    p = ctypes.c_void_p(0x1000)
+    for f in (L.dllm_quantize_int8, L.dllm_quantize_q4_0):
+        assert f(None, dl.DLLM_BF16, 4, 4, p, p, None) == dl.DLLM_E_INVAL
+        assert f(p, dl.DLLM_BF16, 0, 4, p, p, None) == dl.DLLM_E_INVAL
+        assert f(p, dl.DLLM_BF16, 4, 0, p, p, None) == dl.DLLM_E_INVAL
+        assert f(p, dl.DLLM_W8, 4, 4, p, p, None) == dl.DLLM_E_DTYPE

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_ids_match_where_decided, assert_logits_close, dev_i32, gpu_logits, gpu_step, tol
+from gpu_util import assert_ids_match_where_decided, assert_logits_close, dev_i32, dev_u8, gpu_logits, gpu_step, tol
 
 pytestmark = pytest.mark.gpu
 
@@ -24,8 +24,30 @@ import paper_2606_13740_amd as dl  # noqa: E402
 BIG = synth.LLADA_8B
 
 
-def _run(shape, dtype, P, W, masked, cap_extra=0):
-    print(f"case: 8B-width {dtype}, layers {shape.n_layers}, prefix {P}, window {W}", flush=True)
+def _host_gib_available():
+    try:
+        import psutil
+        return psutil.virtual_memory().available / 2**30
+    except Exception:
+        return 0.0
+
+
+def _sls_step(model, kv, tok, mask, n_need):
+    """The benchmark's speculative-window call: dllm_denoise_window_sls at w0 = P with
+    the mask as the need flags (only masked rows get an LM-head output)."""
+    W = len(tok)
+    ids = torch.empty(W, dtype=torch.int32, device="cuda")
+    conf = torch.empty(W, device="cuda")
+    d_mask = dev_u8(mask)
+    dl.dllm_denoise_window_sls(model.handle, kv.handle, kv.prefix_len, dev_i32(tok), d_mask, d_mask, n_need, W,
+                               ids, conf)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), conf.cpu().numpy().astype(np.float64)
+
+
+def _run(shape, dtype, P, W, masked, cap_extra=0, sls=False):
+    print(f"case: 8B-width {dtype}, layers {shape.n_layers}, prefix {P}, window {W}"
+          f"{', selective logits' if sls else ''}", flush=True)
     layers = [synth.layer_weights(shape, l, "bf16") for l in range(shape.n_layers)]
     glob = synth.global_weights(shape, "bf16")
     model = dl.Model(shape, dtype, glob, lambda l: layers[l], max_window=64, max_pos=P + W + 64)
@@ -35,9 +57,18 @@ def _run(shape, dtype, P, W, masked, cap_extra=0):
     tok, mask = synth.window(shape, W, masked)
     logits, ids, conf = gpu_logits(model, kv, tok, mask)
     s_ids, s_conf = gpu_step(model, kv, tok, mask)
+    if sls:
+        l_ids, l_conf = _sls_step(model, kv, tok, mask, len(masked))
+        kept = mask != 0
+        np.testing.assert_array_equal(l_ids[kept], ids[kept])
+        np.testing.assert_allclose(l_conf[kept], conf[kept], rtol=1e-5, atol=0)
+        assert np.all(l_ids[~kept] == -1) and np.all(l_conf[~kept] == 0.0)
     print("  gpu done; oracle ...", flush=True)
+    # the float64 oracle converts a layer's weights on each use; keep them when the host
+    # has room for all of them (the quantised paths convert slowly)
+    cache = shape.params_per_layer * shape.n_layers * 8 < (_host_gib_available() - 48) * 2**30
     om = oracle.OracleModel(shape, dict(glob, layers=layers), int8=(dtype == "w8"), q4=(dtype == "q4"),
-                            cache_layers=False)
+                            cache_layers=cache)
     okv = oracle.OracleKV(shape, P + W + cap_extra)
     oracle.prefill(om, okv, prompt)
     ref = oracle.denoise_step(om, okv, tok, mask)
@@ -75,3 +106,28 @@ def test_8b_width_long_prefix_int8_spec_window():
 @pytest.mark.timeout(900)
 def test_8b_full_depth_step():
     _run(BIG, "bf16", 512, 32, list(range(8, 32)))
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_8b_full_depth_int8_spec_window_sls():
+    """32 layers of int8 weights, a 64-row all-MASK window (current + speculative
+    block) through the benchmark's selective-logits call, prefix 512."""
+    _run(BIG, "w8", 512, 64, list(range(0, 64)), sls=True)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_8b_width_int8_prefix_4096_spec_window():
+    """The long-prefix int8 workload's launches at its own prefix: 4096 keys + the
+    64-row window = 130 key blocks in 15 attention splits, through the selective-logits
+    call the benchmark makes.  Two layers (the oracle's 4096-token prefill is the cost)."""
+    _run(BIG.with_layers(2), "w8", 4096, 64, list(range(0, 64)), sls=True)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_8b_full_depth_bf16_spec_window_prefix_1024():
+    """32 layers, bf16, prefix 1024, a 64-row window with 8 MASK in the current block
+    and an all-MASK speculative block, through the selective-logits call."""
+    _run(BIG, "bf16", 1024, 64, list(range(24, 64)), sls=True)

@@ -52,6 +52,8 @@ def test_staged_commit_matches_oracle(n):
         mask = (state == oracle.IV).astype(np.uint8)
         pred = rng.integers(0, 126000, n).astype(np.int32)
         tok = np.where(mask == 1, 126463, rng.integers(0, 126000, n)).astype(np.int32)
+        same = (mask == 0) & (rng.random(n) < 0.5)          # visible rows predicting their held id
+        tok[same] = pred[same]
         b = int(rng.integers(0, n))
         ln = int(rng.integers(1, n - b + 1))
         tv = float(rng.choice([0.0, 0.25, 0.7, 1.5]))
@@ -98,17 +100,19 @@ def test_staged_generation_loop(dtype):
         dl.dllm_append_prefix_kv(model.handle, kv.handle, dev_i32(tok), B)
 
 
-def test_staged_generator_cache_parity():
+@pytest.mark.parametrize("max_window", [64, 32])
+def test_staged_generator_matches_oracle_repredict(max_window):
     """The host driver (paper_2606_13740_amd.staged): blocks decoded with staged
-    commits, appended with their visible tokens, then the two-phase re-prediction
-    refresh.  Its decisions are replayed in the oracle (same appends, same refresh
-    chunks with the same ids) and the whole GPU cache must match the oracle's; the
-    refresh decisions must match the oracle's confidences wherever they are not within
-    rounding of a threshold."""
+    commits and appended with their visible tokens, then the re-prediction of every
+    tracked position.  The oracle replays the same appends and runs its own
+    re-prediction rule (oracle.repredict_tracked) from the same tracked set: the
+    positions that became stable, the ids written back and the whole cache must match.
+    With max_window 64 the driver shares one refresh between a block's write-back and
+    the next block's re-prediction; with 32 it cannot, and the result is the same."""
     from paper_2606_13740_amd.staged import StagedGenerator
 
     sh = synth.TINY
-    model, om, _ = build_pair(sh, "f32", max_pos=512)
+    model, om, _ = build_pair(sh, "f32", max_window=max_window, max_pos=512)
     P0, B, nb = 64, sh.block, 3
     kv = dl.KVCache(model, P0 + nb * B)
     prompt = synth.prompt_ids(sh, P0)
@@ -122,7 +126,7 @@ def test_staged_generator_cache_parity():
     ts_blocks = [2.0, gen.ts, gen.ts]        # block 0 keeps every promoted token visible
     n_prom = 0
     for b in range(nb):
-        print(f"case: staged generator block {b}", flush=True)
+        print(f"case: staged generator block {b}, max_window {max_window}", flush=True)
         gen.ts = ts_blocks[b]
         t, st = gen.block()
         assert np.all(st != oracle.IV) and gen.steps[-1] <= B
@@ -132,27 +136,38 @@ def test_staged_generator_cache_parity():
         assert sorted(np.concatenate(block_prom).tolist()) == list(range(B))     # each position once
         oracle.append_block(om, okv, t)
     assert len(gen.tracked) >= B, "block 0's tokens all stay visible"
-    # re-prediction thresholds that split the refresh confidences
-    pos_all = sorted(gen.tracked)
-    first = pos_all[:model.cfg.max_window]
+    # re-prediction thresholds between observed confidences of the first tracked block
+    first = [p for p in sorted(gen.tracked) if (p - P0) // B == (min(gen.tracked) - P0) // B]
     _, c_probe, _ = oracle.refresh(om, okv.copy(), first, [sh.mask_id] * len(first))
-    gen.tv, gen.ts = float(np.quantile(c_probe, 0.3)), float(np.quantile(c_probe, 0.7))
+    c = np.sort(c_probe.astype(np.float32))
+    i1, i2 = len(c) // 3, 2 * len(c) // 3
+    gen.tv, gen.ts = float((c[i1 - 1] + c[i1]) / 2), float((c[i2 - 1] + c[i2]) / 2)
     tracked_before = dict(gen.tracked)
     stable, chosen = gen.refresh_visible()
-    assert set(chosen) == set(tracked_before) and not (set(stable) & set(gen.tracked))
-    for c0 in range(0, len(pos_all), model.cfg.max_window):
-        pos = pos_all[c0:c0 + model.cfg.max_window]
-        r_ids, r_conf, _ = oracle.refresh(om, okv, pos, [sh.mask_id] * len(pos))
-        oracle.refresh(om, okv, pos, [chosen[p] for p in pos], lm_head=False)
-        for j, p in enumerate(pos):
-            c = np.float32(r_conf[j])
-            if abs(float(c) - gen.ts) > 1e-6 and abs(float(c) - gen.tv) > 1e-6:
-                want = r_ids[j] if c >= np.float32(gen.tv) else tracked_before[p]
-                assert chosen[p] == want, (p, chosen[p], want, float(c))
-                assert (p in stable) == bool(c >= np.float32(gen.ts))
+    o_tracked = dict(tracked_before)
+    o_stable, o_chosen = oracle.repredict_tracked(om, okv, o_tracked, gen.tv, gen.ts)
+    print(f"  tracked {len(tracked_before)}, stable {len(stable)}, "
+          f"changed ids {sum(chosen[p] != tracked_before[p] for p in chosen)}", flush=True)
+    assert stable == o_stable
+    assert chosen == o_chosen
+    assert gen.tracked == o_tracked
+    assert 0 < len(stable) < len(tracked_before)
     K, Vt = kv.views()
     n = okv.prefix_len
     Kg = K.cpu().numpy()[:, :, :n, :]
     Vg = np.swapaxes(Vt.cpu().numpy()[:, :, :, :n], 2, 3)
     np.testing.assert_allclose(Kg, np.transpose(okv.K[:, :n], (0, 2, 1, 3)), atol=2e-4, rtol=0)
     np.testing.assert_allclose(Vg, np.transpose(okv.V[:, :n], (0, 2, 1, 3)), atol=2e-4, rtol=0)
+
+
+def test_staged_commit_keeps_a_visible_token_whose_prediction_moved():
+    """The GPU kernel's stability rule is the held token's: a visible position whose
+    step predicts another id stays visible at any confidence."""
+    conf = np.array([0.95, 0.95, 0.95, 0.10], np.float32)
+    pred = np.array([5, 6, 7, 8], np.int32)
+    tok = np.array([4, 6, 99, 99], np.int32)
+    mask = np.array([0, 0, 1, 1], np.uint8)
+    state = np.array([oracle.V, oracle.V, oracle.IV, oracle.IV], np.uint8)
+    got = _run_gpu(conf, pred, tok, mask, state, 0, 4, 0.7, 0.9)
+    assert got[2].tolist() == [oracle.V, oracle.S, oracle.S, oracle.IV]
+    assert got[0].tolist() == [4, 6, 7, 99] and got[1].tolist() == [0, 0, 0, 1] and got[3].tolist() == [2]

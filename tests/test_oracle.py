@@ -7,6 +7,7 @@ index, or a transposed operand anywhere in the oracle.
 """
 import dataclasses
 import itertools
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -486,7 +487,80 @@ def test_int8_quantiser_bounds():
     assert np.all(q[3] == 0) and s[3] == 0
     err = np.abs(w.astype(np.float64) - oracle.dequantize_rows(q, s))
     assert np.all(err <= s[:, None].astype(np.float64) * (0.5 + 2e-5))   # w / s is itself rounded in float32
-    np.testing.assert_array_equal(s[nz], np.abs(w[nz]).max(axis=1) / np.float32(127))
+
+
+# Exact rational arithmetic: an IEEE float32 operation is the exact result rounded to
+# 24 significant bits, ties to even (normal range).  These helpers state that rule with
+# fractions.Fraction, independently of numpy's float32 arithmetic.
+def _round_half_even(fr: Fraction) -> int:
+    n = fr.numerator // fr.denominator
+    r = fr - n
+    if r > Fraction(1, 2) or (r == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return n
+
+
+def _to_f32(fr: Fraction) -> Fraction:
+    if fr == 0:
+        return Fraction(0)
+    a = abs(fr)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    assert e >= -126, "subnormal results are not needed here"
+    ulp = Fraction(2) ** (e - 23)
+    return (1 if fr > 0 else -1) * _round_half_even(a / ulp) * ulp
+
+
+def _int8_code_exact(w: float, amax: float) -> int:
+    s = _to_f32(Fraction(amax) / 127)
+    return max(-127, min(127, _round_half_even(_to_f32(Fraction(w) / s))))
+
+
+def test_int8_quantiser_rounds_half_to_even():
+    """A row whose extreme is 127 has the scale 1 exactly, so w / s = w: codes of
+    values halfway between integers follow round-half-to-even.  Round-half-away
+    would give 1, 3, -1, -3, 127 for the second, fourth, fifth, sixth and last
+    entries."""
+    w = np.array([[127.0, 0.5, 1.5, 2.5, -0.5, -2.5, 3.5, -126.5]], np.float32)
+    q, s = oracle.quantize_rows_int8(w)
+    assert s[0] == np.float32(1.0)
+    assert q[0].tolist() == [127, 0, 2, 2, 0, -2, 4, -126]
+
+
+def test_int8_quantiser_divides_in_float32():
+    """Values next to a rounding boundary: the code is round-half-even of the
+    float32-rounded quotient w / s, with s = float32(max|w| / 127).  The expected
+    codes come from exact rational arithmetic.  Rows are built so that, for several
+    entries, a float64 division (w / s in float64, or s itself kept in float64) would
+    round to the other integer; the test requires that such entries exist."""
+    rng = np.random.default_rng(11)
+    rows, discriminating = [], 0
+    for _ in range(60):
+        amax = np.float32(rng.uniform(0.01, 0.1))
+        s32 = np.float32(amax / np.float32(127))
+        row = [amax]
+        for k in rng.integers(-120, 120, 24):
+            centre = np.float32((k + 0.5) * float(s32))
+            w = centre
+            for step in rng.integers(-3, 4, 1):
+                for _ in range(abs(int(step))):
+                    w = np.nextafter(w, np.float32(np.inf if step > 0 else -np.inf), dtype=np.float32)
+            row.append(w)
+            exact = _int8_code_exact(float(w), float(amax))
+            via64 = int(np.clip(np.rint(float(w) / (float(amax) / 127.0)), -127, 127))
+            via64s32 = int(np.clip(np.rint(float(w) / float(s32)), -127, 127))
+            discriminating += int(exact != via64 or exact != via64s32)
+        rows.append(row)
+    w = np.array(rows, np.float32)
+    q, s = oracle.quantize_rows_int8(w)
+    for i in range(w.shape[0]):
+        assert Fraction(float(s[i])) == _to_f32(Fraction(float(w[i, 0])) / 127)
+        want = [_int8_code_exact(float(v), float(w[i, 0])) for v in w[i]]
+        assert q[i].tolist() == want, i
+    assert discriminating >= 20, discriminating
 
 
 def test_int8_model_is_bf16_model_with_dequantised_weights():
@@ -607,6 +681,8 @@ def _staged_case(rng, n, ties=False):
     mask = (state == oracle.IV).astype(np.uint8)
     pred = rng.integers(0, 1000, n).astype(np.int32)
     tok = np.where(mask == 1, 999, rng.integers(0, 1000, n)).astype(np.int32)
+    same = (mask == 0) & (rng.random(n) < 0.5)          # visible rows whose prediction is the held id
+    tok[same] = pred[same]
     return conf, pred, tok, mask, state
 
 
@@ -639,10 +715,27 @@ def test_commit_staged_postconditions(seed):
     assert np.array_equal(tok, np.where(prom, pred, tok0))
     assert np.array_equal(mask, np.where(prom, 0, mask0))
     vis_after = prom | (state0 == oracle.V)
-    want_state = np.where(seg & vis_after & (conf >= np.float32(ts)), oracle.S,
+    holds = tok == pred                                         # the step predicts the held id
+    want_state = np.where(seg & vis_after & holds & (conf >= np.float32(ts)), oracle.S,
                           np.where(prom, oracle.V, state0))
     assert np.array_equal(state, want_state.astype(np.uint8))
     assert np.all(state >= state0)                             # states only move forward
+
+
+def test_commit_staged_stability_is_a_property_of_the_held_token():
+    """A visible token becomes stable only if the step predicts that token: a row that
+    now predicts another id at 0.95 keeps its token and stays visible (tracked for
+    revision); the same confidence on the held id makes it stable, and a position
+    promoted in this step holds its prediction by construction."""
+    conf = np.array([0.95, 0.95, 0.95, 0.10], np.float32)
+    pred = np.array([5, 6, 7, 8], np.int32)
+    tok = np.array([4, 6, 99, 99], np.int32)                # row 0 holds 4 but predicts 5
+    mask = np.array([0, 0, 1, 1], np.uint8)
+    state = np.array([oracle.V, oracle.V, oracle.IV, oracle.IV], np.uint8)
+    got = oracle.commit_staged(conf, pred, tok, mask, state, 0, 4, 0.7, 0.9)
+    assert got.tolist() == [2]
+    assert state.tolist() == [oracle.V, oracle.S, oracle.S, oracle.IV]
+    assert tok.tolist() == [4, 6, 7, 99] and mask.tolist() == [0, 0, 0, 1]
 
 
 def test_commit_staged_high_threshold_is_top1_commit():
@@ -689,3 +782,111 @@ def test_commit_staged_progress_and_stability():
         if not mask.any():
             break
     assert not mask.any() and np.all(state != oracle.IV)
+
+
+# ---- re-prediction of tracked visible prefix tokens ----
+
+STS_SHAPE = dataclasses.replace(MICRO, block=4)
+
+
+def _sts_prefix(seed=5, P0=8, nb=3):
+    """Oracle model, a cache with a prompt and nb appended blocks of random ids, and
+    the whole id sequence."""
+    sh = STS_SHAPE
+    m, _ = micro_model(sh, seed=seed)
+    rng = np.random.default_rng(seed)
+    seq = rng.integers(0, sh.mask_id, P0 + nb * sh.block).astype(np.int32)
+    kv = oracle.OracleKV(sh, len(seq))
+    oracle.prefill(m, kv, seq[:P0])
+    for b in range(nb):
+        oracle.append_block(m, kv, seq[P0 + b * sh.block:P0 + (b + 1) * sh.block])
+    return m, kv, seq, P0
+
+
+def _brute_conf(m, seq, P0, masked):
+    """(id, conf) of every position from one full block-causal forward of seq with the
+    given positions set to MASK, plus that forward's K/V."""
+    s = seq.copy()
+    s[list(masked)] = m.shape.mask_id
+    allowed = oracle.block_causal_allowed(len(s), P0, m.shape.block)
+    _, logits, K, V = oracle.forward_full(m, s, allowed)
+    ids, conf = oracle.confidence(logits)
+    return ids, conf, K, V
+
+
+def test_repredict_trailing_blocks_equals_sequential_brute_force():
+    """When the tracked set is every position of the last blocks, each block's
+    re-prediction sees only fresh K/V, so it equals a full recompute: block b's (id,
+    conf) are those of a full block-causal forward with the earlier tracked blocks at
+    their new ids and block b hidden (MASK), and the cache afterwards equals a full
+    recompute of the final sequence.  A variant that masks more than one block at a
+    time (chunks of a fixed row count) or that re-predicts a block before the previous
+    one is written back fails this."""
+    m, kv, seq, P0 = _sts_prefix()
+    B = m.shape.block
+    blocks = [list(range(P0 + b * B, P0 + (b + 1) * B)) for b in (1, 2)]
+    tracked = {p: int(seq[p]) for blk in blocks for p in blk}
+    ids1, conf1, _, _ = _brute_conf(m, seq, P0, blocks[0])
+    c = np.sort(conf1[blocks[0]].astype(np.float32))
+    tv, ts = float((c[0] + c[1]) / 2), float((c[2] + c[3]) / 2)   # between observed values: no ties
+    stable, chosen = oracle.repredict_tracked(m, kv, dict(tracked), tv, ts)
+    want, cur, want_stable = {}, seq.copy(), []
+    for blk in blocks:
+        ids, conf, _, _ = _brute_conf(m, cur, P0, blk)
+        for p in blk:
+            cf = np.float32(conf[p])
+            want[p] = int(ids[p]) if cf >= np.float32(tv) else int(cur[p])
+            if cf >= np.float32(ts):
+                want_stable.append(p)
+        for p in blk:
+            cur[p] = want[p]
+    assert chosen == want and stable == sorted(want_stable)
+    assert 0 < len(stable) < 2 * B and any(want[p] != seq[p] for p in want)    # every branch taken
+    _, _, K, V = _brute_conf(m, cur, P0, [])
+    np.testing.assert_allclose(kv.K[:, :len(seq)], K, atol=1e-10, rtol=0)
+    np.testing.assert_allclose(kv.V[:, :len(seq)], V, atol=1e-10, rtol=0)
+
+
+def test_repredict_updates_tracking_and_touches_only_tracked_rows():
+    """Stable positions leave the tracked set; the others keep the id written back;
+    cache rows of untracked positions are unchanged; the thresholds split the
+    decisions exactly as stated (conf >= theta_stable -> new id and stable,
+    conf >= theta_visible -> new id, otherwise the held id)."""
+    m, kv, seq, P0 = _sts_prefix(seed=9, nb=3)
+    B = m.shape.block
+    tracked = {P0 + 1: int(seq[P0 + 1]), P0 + 3: int(seq[P0 + 3]), P0 + B + 2: int(seq[P0 + B + 2]),
+               P0 + 2 * B: int(seq[P0 + 2 * B]), P0 + 2 * B + 3: int(seq[P0 + 2 * B + 3])}
+    K0, V0 = kv.K.copy(), kv.V.copy()
+    # every position stays: thresholds above 1 keep every held id
+    t = dict(tracked)
+    stable, chosen = oracle.repredict_tracked(m, kv.copy(), t, 2.0, 3.0)
+    assert stable == [] and chosen == tracked and t == tracked
+    # theta_visible 0: every position takes its re-predicted id; theta_stable 0: all stable
+    t = dict(tracked)
+    kv2 = kv.copy()
+    stable, chosen = oracle.repredict_tracked(m, kv2, t, 0.0, 0.0)
+    assert stable == sorted(tracked) and t == {} and set(chosen) == set(tracked)
+    assert all(c != m.shape.mask_id for c in chosen.values())
+    untracked = [p for p in range(len(seq)) if p not in tracked]
+    np.testing.assert_array_equal(kv2.K[:, untracked], K0[:, untracked])
+    np.testing.assert_array_equal(kv2.V[:, untracked], V0[:, untracked])
+
+
+def test_refresh_of_a_block_and_the_next_block_equals_two_refreshes():
+    """The sparse refresh lets two consecutive blocks share one call: rows of block b
+    see keys only up to the end of block b, so refreshing block b's rows together with
+    block b + 1's rows gives block b's rows the results of a refresh of block b alone,
+    and block b + 1's rows those of a second refresh made after it.  (The GPU driver
+    merges the write-back of one block with the re-prediction of the next this way.)"""
+    m, kv, seq, P0 = _sts_prefix(seed=4, nb=3)
+    B, mask_id = m.shape.block, m.shape.mask_id
+    wb_pos, wb_ids = [P0 + B + 1, P0 + B + 2], [3, 17]
+    mk_pos = [P0 + 2 * B, P0 + 2 * B + 2, P0 + 2 * B + 3]
+    kv_a, kv_b = kv.copy(), kv.copy()
+    ia, ca, _ = oracle.refresh(m, kv_a, wb_pos + mk_pos, wb_ids + [mask_id] * 3)
+    ib1, cb1, _ = oracle.refresh(m, kv_b, wb_pos, wb_ids)
+    ib2, cb2, _ = oracle.refresh(m, kv_b, mk_pos, [mask_id] * 3)
+    np.testing.assert_array_equal(ia, np.concatenate([ib1, ib2]))
+    np.testing.assert_allclose(ca, np.concatenate([cb1, cb2]), rtol=1e-12)
+    np.testing.assert_allclose(kv_a.K, kv_b.K, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(kv_a.V, kv_b.V, atol=1e-12, rtol=0)
