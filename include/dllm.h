@@ -181,6 +181,25 @@ int dllm_prefill(dllm_model* m, dllm_kv* kv, const int32_t* d_ids, int32_t n, dl
 int dllm_denoise_step(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask,
                       int32_t W, int32_t* d_out_id, float* d_out_conf, dllm_stream stream);
 
+/* dllm_denoise_step for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, checks and results as dllm_denoise_step, but the step's scratch (the
+ * residual stream, activation fragments, split-K, attention and LM-head partials)
+ * is carved from a static device array of the library (64 MiB per device, held until
+ * the process ends) instead of the model's workspace; the call itself allocates and
+ * frees nothing.  The array's device address is resolved once per device (at
+ * dllm_model_create, or at the first call on a device).  Every call on a device
+ * shares that device's array and leaves the last call's contents in it: calls that
+ * overlap on one device (concurrent streams, threads, or this call beside another
+ * model's) race.  Each call first clears what must be zero (the padding columns of
+ * its activation fragments, when d_model or d_ff is not a whole number of 32- or
+ * 64-column chunks; no launch otherwise); every other buffer the step reads is
+ * written by the same step first, or feeds only padding rows.  E_CAPACITY if the
+ * step's scratch for this model and W exceeds 64 MiB (LLaDA-8B and Dream-7B widths
+ * need about 40 MiB at W <= 64), plus dllm_denoise_step's errors. */
+int dllm_denoise_step_noalloc(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
+                              int32_t* d_out_id, float* d_out_conf, dllm_stream stream);
+
 /* Confidence-selected commit over one segment (Background: "updates a
  * confidence-selected subset"; a draft segment is committed separately, System
  * Design, "Multi-Block Speculative Decoding").  Among the positions p in

@@ -64,6 +64,7 @@ _SIGNATURES = {
     "dllm_commit": ([_vp, _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_append_prefix_kv": ([_vp, _vp, _vp, _i32, _vp], ctypes.c_int),
     "dllm_refresh_kv": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "dllm_denoise_step_noalloc": ([_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_denoise_window": ([_vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_denoise_window_sls": ([_vp, _vp, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp], ctypes.c_int),
     "dllm_accept_drafts": ([_vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _vp, _vp, _vp], ctypes.c_int),
@@ -168,6 +169,11 @@ def dllm_prefill(model: int, kv: int, ids, n: int, stream=None):
 def dllm_denoise_step(model: int, kv: int, tok, mask, W: int, out_id, out_conf, stream=None):
     _check(lib().dllm_denoise_step(model, kv, _ptr(tok), _ptr(mask), W, _ptr(out_id), _ptr(out_conf),
                                    _stream(stream)), "dllm_denoise_step")
+
+
+def dllm_denoise_step_noalloc(model: int, kv: int, tok, mask, W: int, out_id, out_conf, stream=None):
+    _check(lib().dllm_denoise_step_noalloc(model, kv, _ptr(tok), _ptr(mask), W, _ptr(out_id), _ptr(out_conf),
+                                           _stream(stream)), "dllm_denoise_step_noalloc")
 
 
 def dllm_commit(conf, ids, tok, mask, seg_begin: int, seg_len: int, k: int, committed_pos=None,

@@ -12,7 +12,9 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/dllm.h"
@@ -64,6 +66,7 @@ struct LayerW {
 };
 
 struct Workspace {
+    void* block = nullptr;   // the one device allocation the buffers below are carved from
     int rows = 0;            // token rows (multiple of 64)
     int wrows = 0;           // window rows for LM / attention partials (multiple of 64)
     float* x = nullptr;      // [rows][d]
@@ -344,9 +347,7 @@ struct ProbeScope {
 // ---------------------------------------------------------------------------
 
 void free_ws(Workspace& w) {
-    void* ptrs[] = {w.x, w.xg, w.q, w.of, w.af, w.pos, w.lim, w.lm, w.part, w.opart, w.mlpart, w.tok, w.msk, w.oid, w.oconf, w.need};
-    for (void* p : ptrs)
-        if (p) (void)hipFree(p);
+    if (w.block) (void)hipFree(w.block);
     w = Workspace{};
 }
 
@@ -359,46 +360,76 @@ int alloc_zero(void** p, size_t bytes) {
     return DLLM_OK;
 }
 
+// The buffers of a workspace for `rows` token rows (a multiple of 64), LM-head and
+// attention partials for `wrows` rows, and `part_floats` split-K partials, laid out
+// one after another (256-byte aligned) from `base`.  Returns the bytes they take; with
+// base == nullptr only the size is computed.  Every user of a workspace (the model's
+// own, grown on demand, and the no-allocation step's static scratch) is carved here.
+size_t ws_carve(const dllm_model* m, int rows, int wrows, size_t part_floats, char* base, Workspace* w);
+
+// Split-K partials: 4 slices of the window rows (streaming layouts), or up to 8 slices
+// of 256+ token rows (tiled layout), at most 4096 rows.
+size_t part_floats_for(const dllm_model* m, int rows, int wrows) {
+    return (size_t)std::max({RES_SPLIT * wrows, rows, std::min(8 * rows, 4096)}) * m->cfg.d_model;
+}
+
 int ensure_ws(dllm_model* m, int rows_needed) {
     const dllm_config& c = m->cfg;
     const int rows = (int)round_up(std::max(rows_needed, 1), 64);
-    if (m->ws.rows >= rows && m->ws.x) return DLLM_OK;
+    if (m->ws.rows >= rows && m->ws.block) return DLLM_OK;
     HIP_TRY(hipDeviceSynchronize());
     free_ws(m->ws);
-    Workspace& w = m->ws;
-    w.rows = rows;
-    w.wrows = (int)round_up(c.max_window, 64);
-    const size_t d = c.d_model;
-    int rc;
-#define ALLOC(ptr, bytes) \
-    if ((rc = alloc_zero((void**)&(ptr), (bytes))) != DLLM_OK) { free_ws(w); return rc; }
-    ALLOC(w.x, (size_t)rows * d * 4);
-    const size_t xchunk = m->xf32 ? 1024 : 2048;   // an activation chunk: fp32, or bf16 hi + lo
-    w.xg_bytes = w.of_bytes = (size_t)(rows / 16) * m->KCx_d * xchunk;
-    w.af_bytes = (size_t)(rows / 16) * m->KCx_f * xchunk;
-    ALLOC(w.xg, w.xg_bytes);
-    ALLOC(w.q, (size_t)rows * d * 4);   // fp32, or bf16 hi and lo planes
-    ALLOC(w.of, w.of_bytes);
-    ALLOC(w.af, w.af_bytes);
-    ALLOC(w.pos, (size_t)rows * 4);
-    ALLOC(w.lim, (size_t)rows * 4);
-    ALLOC(w.lm, (size_t)m->n_lm_wg * w.wrows * sizeof(LmPartial));
-    w.part_floats = (size_t)std::max({RES_SPLIT * w.wrows, rows, std::min(8 * rows, 4096)}) * d;
-    ALLOC(w.part, w.part_floats * 4);
-    ALLOC(w.opart, (size_t)MAX_SPLIT * w.wrows * d * 4);
-    ALLOC(w.mlpart, (size_t)MAX_SPLIT * w.wrows * c.n_heads * 2 * 4);
-    ALLOC(w.tok, (size_t)rows * 4);
-    ALLOC(w.msk, (size_t)rows);
-    ALLOC(w.oid, (size_t)rows * 4);
-    ALLOC(w.oconf, (size_t)rows * 4);
-    ALLOC(w.need, (size_t)rows);
-#undef ALLOC
+    const int wrows = (int)round_up(c.max_window, 64);
+    const size_t part_floats = part_floats_for(m, rows, wrows);
+    const size_t bytes = ws_carve(m, rows, wrows, part_floats, nullptr, nullptr);
+    void* blk = nullptr;
+    int rc = alloc_zero(&blk, bytes);
+    if (rc) return rc;
+    ws_carve(m, rows, wrows, part_floats, (char*)blk, &m->ws);
+    m->ws.block = blk;
     return DLLM_OK;
 }
 
 // ---------------------------------------------------------------------------
 // Weight prepacking
 // ---------------------------------------------------------------------------
+
+size_t ws_carve(const dllm_model* m, int rows, int wrows, size_t part_floats, char* base, Workspace* w) {
+    const dllm_config& c = m->cfg;
+    const size_t d = c.d_model;
+    const size_t xchunk = m->xf32 ? 1024 : 2048;   // an activation chunk: fp32, or bf16 hi + lo
+    const size_t xg_bytes = (size_t)(rows / 16) * m->KCx_d * xchunk;
+    const size_t af_bytes = (size_t)(rows / 16) * m->KCx_f * xchunk;
+    size_t off = 0;
+    auto take = [&](auto*& ptr, size_t bytes) {
+        if (base) ptr = (std::remove_reference_t<decltype(ptr)>)(base + off);
+        off += round_up((long)std::max<size_t>(bytes, 1), 256);
+    };
+    Workspace tmp;
+    Workspace& v = w ? *w : tmp;
+    v.rows = rows;
+    v.wrows = wrows;
+    v.xg_bytes = v.of_bytes = xg_bytes;
+    v.af_bytes = af_bytes;
+    v.part_floats = part_floats;
+    take(v.x, (size_t)rows * d * 4);
+    take(v.xg, xg_bytes);
+    take(v.q, (size_t)rows * d * 4);   // fp32, or bf16 hi and lo planes
+    take(v.of, xg_bytes);
+    take(v.af, af_bytes);
+    take(v.pos, (size_t)rows * 4);
+    take(v.lim, (size_t)rows * 4);
+    take(v.lm, (size_t)m->n_lm_wg * wrows * sizeof(LmPartial));
+    take(v.part, part_floats * 4);
+    take(v.opart, (size_t)MAX_SPLIT * wrows * d * 4);
+    take(v.mlpart, (size_t)MAX_SPLIT * wrows * c.n_heads * 2 * 4);
+    take(v.tok, (size_t)rows * 4);
+    take(v.msk, (size_t)rows);
+    take(v.oid, (size_t)rows * 4);
+    take(v.oconf, (size_t)rows * 4);
+    take(v.need, (size_t)rows);
+    return off;
+}
 
 int kc_of(int wt) { return wt == WT_F32 ? 16 : (wt == WT_BF16 ? 32 : 64); }
 
@@ -483,14 +514,14 @@ struct FwdArgs {
     int n_sel;                // at most this many flagged rows get an LM output
     int replay = -1;          // >= 0: only launch this kernel class, n_replay times (timing)
     int n_replay = 0;
+    Workspace* ws = nullptr;  // a caller-provided workspace (no growth), else the model's
 };
 
 // O / down projection: split-K GEMM into partials, then the reduction that adds
 // them to the residual and prepares the next RMSNorm's operand and partial sums.
 template <int WT, bool XF32>
-int residual_proj(dllm_model* m, const PackedW& W, const void* X, const float* gnext, int M, int Mc, int MT, int gy,
-                  hipStream_t s, bool sel = false, const uint8_t* need = nullptr, int n_sel = 0) {
-    Workspace& w = m->ws;
+int residual_proj(dllm_model* m, Workspace& w, const PackedW& W, const void* X, const float* gnext, int M, int Mc,
+                  int MT, int gy, hipStream_t s, bool sel = false, const uint8_t* need = nullptr, int n_sel = 0) {
     const int d = m->cfg.d_model;
     const Decomp dc = decomp(G_RES, WT, W.n_tiles, Mc, gy);
     const int KS = dc.ks;
@@ -510,9 +541,9 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     constexpr bool XF32 = (WT == WT_F32);
     const dllm_config& c = m->cfg;
     const int d = c.d_model, H = c.n_heads, Dh = c.head_dim;
-    int rc = ensure_ws(m, a.M);
+    int rc = a.ws ? DLLM_OK : ensure_ws(m, a.M);
     if (rc) return rc;
-    Workspace& w = m->ws;
+    Workspace& w = a.ws ? *a.ws : m->ws;
 
     int MT, gy;
     if (a.M <= 64) { MT = pick_MT(a.M); gy = 1; }
@@ -604,7 +635,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         // O projection + residual (+ the norm-2 operand)
         if (run(DLLM_K_OPROJ)) {
             ProbeScope ps(m, DLLM_K_OPROJ, s);
-            if ((rc = residual_proj<WT, XF32>(m, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) return rc;
+            if ((rc = residual_proj<WT, XF32>(m, w, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) return rc;
         }
         // RMSNorm + gate/up + SwiGLU
         if (run(DLLM_K_GATEUP)) {
@@ -621,7 +652,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
             const float* gnext = last ? m->gf : m->layers[l + 1].g1;
             const bool sel = last && a.lm && a.sel;
             ProbeScope ps(m, DLLM_K_DOWN, s);
-            if ((rc = residual_proj<WT, XF32>(m, L.down, w.af, gnext, a.M, Mc, MT, gy, s, sel, a.need, a.n_sel)))
+            if ((rc = residual_proj<WT, XF32>(m, w, L.down, w.af, gnext, a.M, Mc, MT, gy, s, sel, a.need, a.n_sel)))
                 return rc;
         }
     }
@@ -666,6 +697,40 @@ int check_model_kv(const dllm_model* m, const dllm_kv* kv) {
     if (!m) return fail(DLLM_E_INVAL, "model is NULL");
     if (!kv) return fail(DLLM_E_INVAL, "kv is NULL");
     if (kv->model != m) return fail(DLLM_E_INVAL, "kv cache belongs to another model");
+    return DLLM_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Static scratch of the no-allocation step (dllm_denoise_step_noalloc): the step's
+// workspaces carved from this array instead of the model's.  Each device holds its
+// own copy (at its own address) until the process ends.  Host code never passes
+// the array's name to a kernel: it resolves the device address once per device with
+// hipGetSymbolAddress and uses that pointer.
+// ---------------------------------------------------------------------------
+static constexpr size_t SCRATCH_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device (resolved on the first call per device).
+int scratch_ptr(void** out) {
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= MAX_DEVICES) return fail(DLLM_E_INVAL, "device index out of range for the static scratch");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(DLLM_E_HIP, "hipGetSymbolAddress returned NULL for the static scratch");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
     return DLLM_OK;
 }
 
@@ -797,6 +862,10 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
         return cleanup(fail(DLLM_E_HIP, "weight prepacking failed"));
     if ((rc = ensure_ws(m, c.max_window))) return cleanup(rc);
+    {
+        void* sp = nullptr;     // resolve the static scratch of this device while it is current
+        if ((rc = scratch_ptr(&sp))) return cleanup(rc);
+    }
     *out = m;
     return DLLM_OK;
 }
@@ -890,6 +959,42 @@ int dllm_denoise_step(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const ui
     FwdArgs a{};
     a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + W;
     a.n_layers = m->cfg.n_layers; a.lm = true; a.out_id = d_out_id; a.out_conf = d_out_conf;
+    return forward(m, kv, a, (hipStream_t)stream);
+}
+
+int dllm_denoise_step_noalloc(dllm_model* m, dllm_kv* kv, const int32_t* d_tok, const uint8_t* d_mask, int32_t W,
+                              int32_t* d_out_id, float* d_out_conf, dllm_stream stream) {
+    int rc = window_checks(m, kv, d_tok, W);
+    if (rc) return rc;
+    if (!d_out_id || !d_out_conf) return fail(DLLM_E_INVAL, "output pointer is NULL");
+    const int rows = (int)round_up(W, 64);
+    const size_t part_floats = part_floats_for(m, rows, rows);
+    const size_t need = ws_carve(m, rows, rows, part_floats, nullptr, nullptr);
+    if (need > SCRATCH_BYTES)
+        return fail(DLLM_E_CAPACITY, "the step needs " + std::to_string(need) + " bytes of scratch; the static scratch holds " +
+                                         std::to_string(SCRATCH_BYTES));
+    void* base = nullptr;
+    if ((rc = scratch_ptr(&base))) return rc;
+    Workspace w;
+    ws_carve(m, rows, rows, part_floats, (char*)base, &w);
+    // padding columns of the activation fragments (widths that are not whole chunks):
+    // never written by the step, multiplied by zero weights, so they must be zeros
+    const int kcol = m->xf32 ? 16 : 32;
+    const struct { void* buf; int KCx, kreal; } pads[] = {
+        {w.xg, m->KCx_d, m->cfg.d_model}, {w.of, m->KCx_d, m->cfg.d_model}, {w.af, m->KCx_f, m->cfg.d_ff}};
+    for (const auto& pd : pads) {
+        if (pd.KCx * kcol == pd.kreal) continue;
+        const long n = (long)(rows / 16) * (pd.KCx - pd.kreal / kcol) * 64 * (m->xf32 ? 1 : 2);
+        if (m->xf32)
+            hipLaunchKernelGGL(zero_frag_pad_kernel<true>, dim3(ceil_div(n, 256)), dim3(256), 0, (hipStream_t)stream,
+                               pd.buf, rows / 16, pd.KCx, pd.kreal);
+        else
+            hipLaunchKernelGGL(zero_frag_pad_kernel<false>, dim3(ceil_div(n, 256)), dim3(256), 0, (hipStream_t)stream,
+                               pd.buf, rows / 16, pd.KCx, pd.kreal);
+    }
+    FwdArgs a{};
+    a.M = W; a.tok = d_tok; a.mask = d_mask; a.pos_base = kv->prefix_len; a.T = kv->prefix_len + W;
+    a.n_layers = m->cfg.n_layers; a.lm = true; a.out_id = d_out_id; a.out_conf = d_out_conf; a.ws = &w;
     return forward(m, kv, a, (hipStream_t)stream);
 }
 

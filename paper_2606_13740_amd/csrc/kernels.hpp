@@ -129,6 +129,36 @@ residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps
     if (dst >= 0) write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, dst, d, eps, g, xg, KCx, red);
 }
 
+// Zeroes the padding columns [kreal, KCx * columns per chunk) of an activation
+// fragment buffer for `tiles` token tiles.  No kernel writes those columns and the
+// GEMMs multiply them by zero weight columns, so they must hold finite values (zeros):
+// a freshly zeroed workspace does, a reused scratch buffer needs this.  One thread per
+// 16-byte lane slot of the chunks that hold padding (bf16 hi/lo: 2 planes).
+template <bool XF32>
+__global__ void __launch_bounds__(256) zero_frag_pad_kernel(void* buf, int tiles, int KCx, int kreal) {
+    constexpr int KCOL = XF32 ? 16 : 32;                  // columns per activation chunk
+    const int kc0 = kreal / KCOL;                          // first chunk holding padding
+    const int nch = KCx - kc0;
+    const int planes = XF32 ? 1 : 2;
+    const long u = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (nch <= 0 || u >= (long)tiles * nch * 64 * planes) return;
+    const int lane = (int)(u % 64);
+    const int pl = (int)((u / 64) % planes);
+    const int c = (int)((u / (64 * planes)) % nch);
+    const int t = (int)(u / (64 * planes * nch));
+    const int kc = kc0 + c, g = lane >> 4;
+    char* p = (char*)buf + (size_t)(t * KCx + kc) * (XF32 ? 1024 : 2048) + pl * 1024 + lane * 16;
+    if (XF32) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+            if (kc * 16 + 4 * s + g >= kreal) ((float*)p)[s] = 0.f;
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (kc * 32 + 8 * g + e >= kreal) ((uint16_t*)p)[e] = 0;
+    }
+}
+
 // Streaming read of n 16-byte units (measurement helper): grid-stride, 4 loads in flight per lane.
 __global__ void __launch_bounds__(256) read_stream_kernel(const u32x4_t* p, size_t n, uint32_t* sink) {
     const size_t stride = (size_t)gridDim.x * blockDim.x;
