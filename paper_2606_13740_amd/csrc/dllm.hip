@@ -81,6 +81,9 @@ struct Workspace {
     size_t part_floats = 0;
     float* opart = nullptr;  // [MAX_SPLIT][wrows][H][Dh]
     float* mlpart = nullptr; // [MAX_SPLIT][wrows][H][2]
+    float* ssq = nullptr;    // [d / 16][rows] sum-of-squares partials of a folded RMSNorm
+    int* slot = nullptr;     // [rows] LM-head slot of each row (selective logits skipping)
+    int ssq_ld = 0;          // partials per row of ssq (a multiple of 64)
     size_t xg_bytes = 0, of_bytes = 0, af_bytes = 0;   // allocated fragment-buffer sizes
     int* tok = nullptr;      // [rows] ids of a merged pass
     uint8_t* msk = nullptr;  // [rows] mask flags of a merged pass
@@ -423,6 +426,9 @@ size_t ws_carve(const dllm_model* m, int rows, int wrows, size_t part_floats, ch
     take(v.part, part_floats * 4);
     take(v.opart, (size_t)MAX_SPLIT * wrows * d * 4);
     take(v.mlpart, (size_t)MAX_SPLIT * wrows * c.n_heads * 2 * 4);
+    v.ssq_ld = (int)round_up(ceil_div(c.d_model, 16), 64);
+    take(v.ssq, (size_t)v.ssq_ld * rows * 4);
+    take(v.slot, (size_t)rows * 4);
     take(v.tok, (size_t)rows * 4);
     take(v.msk, (size_t)rows);
     take(v.oid, (size_t)rows * 4);
@@ -536,6 +542,36 @@ int residual_proj(dllm_model* m, Workspace& w, const PackedW& W, const void* X, 
     return DLLM_OK;
 }
 
+// O / down projection of a window of <= 64 rows with the next RMSNorm folded into
+// the consumer: the whole K range per workgroup (one row tile, 8 waves over K, no
+// split-K partials and no reduction launch); the epilogue updates x, writes the next
+// GEMM's operand x * g_next and one sum-of-squares partial per row tile and token.
+template <int WT, bool XF32>
+int residual_proj_fused(dllm_model* m, Workspace& w, const PackedW& W, const void* X, const float* gnext, int M,
+                        int MT, hipStream_t s, const int* slot = nullptr) {
+    GemmArgs g{W.w, W.scale, X, W.KCw, W.KCw * WTraits<WT>::XPER, W.n_tiles};
+    g.qs = W.qs;
+    g.tpg = 1;
+    EpiResidual<XF32> e{w.x, m->cfg.d_model, M, gnext, w.xg, m->KCx_d, w.ssq, w.ssq_ld, slot};
+    switch (MT) {
+        case 1: launch_gemm_inst<WT, 1, 1, 8, 1>(g, e, W.n_tiles, 1, 1, s); break;
+        case 2: launch_gemm_inst<WT, 1, 1, 8, 2>(g, e, W.n_tiles, 1, 1, s); break;
+        case 3: launch_gemm_inst<WT, 1, 1, 8, 3>(g, e, W.n_tiles, 1, 1, s); break;
+        case 4: launch_gemm_inst<WT, 1, 1, 8, 4>(g, e, W.n_tiles, 1, 1, s); break;
+        default: return fail(DLLM_E_UNIMPL, "unsupported token tile count");
+    }
+    return DLLM_OK;
+}
+
+// The consumer side of a folded RMSNorm: the GEMM sums nssq partials per token.
+void fold_norm(GemmArgs& g, const dllm_model* m, const Workspace& w, int nssq) {
+    g.ssq = w.ssq;
+    g.nssq = nssq;
+    g.ssq_ld = w.ssq_ld;
+    g.dnorm = m->cfg.d_model;
+    g.eps = m->cfg.eps;
+}
+
 template <int WT, typename AT>   // AT: element type of the embedding and the cache planes
 int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
     constexpr bool XF32 = (WT == WT_F32);
@@ -558,13 +594,28 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (a.lm && Mc > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
     }
 
+    // Windows of <= 64 rows fold each RMSNorm into the GEMM that consumes it: the
+    // residual projections update x in their epilogue and leave x * g and per-tile
+    // sums of squares; QKV, gate/up and the LM head scale their outputs per token.
+    // Before a selective LM head (rows packed by need) the last layer writes the final
+    // operand at each kept row's slot, which the embedding kernel records.
+    const bool fused = (gy == 1);
+    // The down projection keeps split-K + the reduction kernel (which writes the
+    // normalised operand): over the whole K range each of its workgroups would read the
+    // whole 12288-wide activation (4x the L2 traffic of 4 split-K slices).  QKV then
+    // reads a normalised operand, except after the embedding (layer 0), which folds.
+    constexpr bool FUSE_DOWN = false;
+    const bool lm_sel_last = a.lm && a.sel;
+    auto nssq_qkv = [&](int l) { return l == 0 ? 1 : m->layers[l - 1].down.n_tiles; };
+
     // replay (timing): the kernels of one class only, with the operands the workspace
     // holds, cycling through the layers
     auto run = [&](int cls) { return a.replay < 0 || a.replay == cls; };
     if (a.replay < 0)
         hipLaunchKernelGGL((embed_kernel<AT, XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const AT*)m->embed, a.tok,
                            a.mask, a.M, d, c.vocab, c.mask_id, c.eps, (const float*)m->layers[0].g1, w.x, w.xg,
-                           m->KCx_d);
+                           m->KCx_d, fused ? w.ssq : nullptr, w.ssq_ld, (fused && lm_sel_last) ? w.slot : nullptr, a.need,
+                           a.n_sel);
 
     // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo]; Hkv heads.
     const size_t plane = (size_t)m->Hkv * kv->Cs * Dh;
@@ -582,6 +633,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (run(DLLM_K_QKV)) {
             GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles, L.bqkv};
             g.qs = L.qkv.qs;
+            if (fused && (l == 0 || FUSE_DOWN)) fold_norm(g, m, w, nssq_qkv(l));
             EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane,
                            kv->Cs};
             ProbeScope ps(m, DLLM_K_QKV, s);
@@ -635,12 +687,17 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         // O projection + residual (+ the norm-2 operand)
         if (run(DLLM_K_OPROJ)) {
             ProbeScope ps(m, DLLM_K_OPROJ, s);
-            if ((rc = residual_proj<WT, XF32>(m, w, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) return rc;
+            if (fused) {
+                if ((rc = residual_proj_fused<WT, XF32>(m, w, L.o, w.of, L.g2, a.M, MT, s))) return rc;
+            } else if ((rc = residual_proj<WT, XF32>(m, w, L.o, w.of, L.g2, a.M, Mc, MT, gy, s))) {
+                return rc;
+            }
         }
         // RMSNorm + gate/up + SwiGLU
         if (run(DLLM_K_GATEUP)) {
             GemmArgs g{L.gu.w, L.gu.scale, w.xg, L.gu.KCw, L.gu.KCw * WTraits<WT>::XPER, L.gu.n_tiles};
             g.qs = L.gu.qs;
+            if (fused) fold_norm(g, m, w, L.o.n_tiles);
             EpiSwiGLU<XF32> e{w.af, m->KCx_f};
             ProbeScope ps(m, DLLM_K_GATEUP, s);
             if ((rc = launch_gemm<WT, G_GU>(decomp(G_GU, WT, L.gu.n_tiles, Mc, gy), L.gu.n_tiles, MT, g, e, gy, s)))
@@ -650,10 +707,15 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (run(DLLM_K_DOWN)) {
             const bool last = (l + 1 == c.n_layers);
             const float* gnext = last ? m->gf : m->layers[l + 1].g1;
-            const bool sel = last && a.lm && a.sel;
+            const bool sel = last && lm_sel_last;
             ProbeScope ps(m, DLLM_K_DOWN, s);
-            if ((rc = residual_proj<WT, XF32>(m, w, L.down, w.af, gnext, a.M, Mc, MT, gy, s, sel, a.need, a.n_sel)))
+            if (fused && FUSE_DOWN) {
+                if ((rc = residual_proj_fused<WT, XF32>(m, w, L.down, w.af, gnext, a.M, MT, s, sel ? w.slot : nullptr)))
+                    return rc;
+            } else if ((rc = residual_proj<WT, XF32>(m, w, L.down, w.af, gnext, a.M, Mc, MT, gy, s, sel, a.need,
+                                                     a.n_sel))) {
                 return rc;
+            }
         }
     }
     if (a.xout) HIP_TRY(hipMemcpyAsync(a.xout, w.x, (size_t)a.M * d * 4, hipMemcpyDeviceToDevice, s));
@@ -668,6 +730,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         if (gyl * MTl * 16 > w.wrows) return fail(DLLM_E_INVAL, "LM head rows exceed the window workspace");
         GemmArgs g{m->lm.w, m->lm.scale, w.xg, m->lm.KCw, m->lm.KCw * WTraits<WT>::XPER, m->lm.n_tiles};
         g.qs = m->lm.qs;
+        if (fused && FUSE_DOWN) fold_norm(g, m, w, m->layers[c.n_layers - 1].down.n_tiles);
         const Decomp dc = decomp(G_LM, WT, m->lm.n_tiles, gyl * MTl * 16, gyl);
         const int gx = row_groups(dc, m->lm.n_tiles);
         if (gx > m->n_lm_wg) return fail(DLLM_E_INVAL, "internal: LM-head partials exceed their buffer");

@@ -31,6 +31,15 @@ struct GemmArgs {
     const float* bias = nullptr;  // per packed row (added after the row scale) or nullptr
     int tpg = 0;          // row tiles per wave group (1 .. FW); the launch sets it
     const uint16_t* qs = nullptr;  // Q4_0: fp16 scales [tile][chunk][16 rows][2 blocks]
+    // RMSNorm folded into the GEMM: the operand X holds x * g (not normalised) and the
+    // producer left per-group partial sums of x^2, ssq[m * ssq_ld + p] for p < nssq
+    // (ssq_ld a multiple of 4); the kernel sums them per token (fixed order) and scales
+    // Y[n][m] by rsqrt(sum / dnorm + eps)
+    const float* ssq = nullptr;
+    int nssq = 0;
+    int ssq_ld = 0;
+    int dnorm = 0;
+    float eps = 0.f;
 };
 
 // Epilogue interface:
@@ -51,6 +60,9 @@ struct GemmArgs {
 template <int WT, int F, int MT>
 constexpr int pipeline_depth() {
     constexpr int XP = (WT == WT_F32) ? 1 : 2;
+    // one row tile per wave (whole-K residual projections): 16 weight stages, the
+    // activations at a quarter to a sixteenth of that depth (activation_depth)
+    if constexpr (F == 1 && (WT == WT_BF16 || WT == WT_I8)) return 16;
     if constexpr (WT == WT_Q4) {
         // code stages: 8-byte codes + a scale dword per tile (3 VGPRs); the
         // activations have their own, shallower pipeline (activation_depth), so the
@@ -77,8 +89,15 @@ constexpr int pipeline_depth() {
 template <int WT, int F, int MT>
 constexpr int activation_depth() {
     if constexpr (WT == WT_Q4) return 1;
+    if constexpr (F == 1 && (WT == WT_BF16 || WT == WT_I8)) {
+        // ~64 VGPRs of activation stages (hi + lo planes, XPER 32-column halves)
+        constexpr int per = 4 * WTraits<WT>::XPER * 2 * MT;
+        constexpr int d = 64 / per;
+        return d >= 8 ? 8 : (d >= 4 ? 4 : (d >= 2 ? 2 : 1));
+    }
     return pipeline_depth<WT, F, MT>();
 }
+
 
 // Reduction slots: the largest power of two <= NWk whose slots fit the budget.
 template <int NWk>
@@ -112,6 +131,7 @@ gemm_kernel(GemmArgs g, Epi epi) {
     __shared__ float Y[NWn][S * SLOT];
     constexpr int ESM = Epi::kSmem > 0 ? Epi::kSmem : 16;
     __shared__ __align__(16) char esm[NWn * ESM];
+    __shared__ float rs_sm[MR];                    // folded RMSNorm: rsqrt(mean x^2 + eps) per token
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -283,6 +303,45 @@ gemm_kernel(GemmArgs g, Epi epi) {
                     wb[s][f] = u32x4_t{0u, 0u, 0u, 0u};
                 }
             }
+        // Folded RMSNorm: each wave sums the partials of tokens wave, wave + NW, ... (one
+        // token per wave at a time): lane l adds partials 4l .. 4l+3 (+ 256 per further
+        // chunk) in order, then a fixed xor tree over the wave, so every workgroup gets
+        // the same bits.  The first four tokens' loads go out before the weight loads
+        // (the waits count loads in issue order, so consuming them later does not wait
+        // for the weight stages).
+        float4 ssq_t[4];
+        auto ssq_load = [&](int j0) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const int j = j0 + b * NW, p = 4 * lane;
+                ssq_t[b] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (j < MR) {
+                    const float* row = g.ssq + (size_t)(mt0 * 16 + j) * g.ssq_ld;
+                    if (p + 3 < g.nssq) {
+                        ssq_t[b] = *(const float4*)(row + p);
+                    } else {
+                        if (p < g.nssq) ssq_t[b].x = row[p];
+                        if (p + 1 < g.nssq) ssq_t[b].y = row[p + 1];
+                        if (p + 2 < g.nssq) ssq_t[b].z = row[p + 2];
+                    }
+                }
+            }
+        };
+        auto ssq_reduce = [&](int j0) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const int j = j0 + b * NW;
+                float v = (ssq_t[b].x + ssq_t[b].y) + (ssq_t[b].z + ssq_t[b].w);
+                for (int c = 256; c < g.nssq; c += 256) {      // d > 4096: further chunks
+                    const float* row = g.ssq + (size_t)(mt0 * 16 + min(j, MR - 1)) * g.ssq_ld + c;
+                    for (int e = 0; e < 4; ++e)
+                        if (j < MR && c + 4 * lane + e < g.nssq) v += row[4 * lane + e];
+                }
+                v = warp_sum(v);
+                if (j < MR && lane == 0) rs_sm[j] = 1.0f / sqrtf(v / (float)g.dnorm + g.eps);
+            }
+        };
+        if (g.ssq != nullptr) ssq_load(wave);
         const bool work = c1 > c0 && nf > 0;
         if (work) {
 #pragma unroll
@@ -292,6 +351,13 @@ gemm_kernel(GemmArgs g, Epi epi) {
             }
         }
         stage_prologue();
+        if (g.ssq != nullptr) {
+            ssq_reduce(wave);
+            for (int j0 = wave + 4 * NW; j0 < MR; j0 += 4 * NW) {
+                ssq_load(j0);
+                ssq_reduce(j0);
+            }
+        }
         if (work) {
             // chunk c uses weight slot c % D and activation slot c % DX (DX divides D).
             // For a group that fills the template, rounds whose D successors all lie
@@ -319,8 +385,13 @@ gemm_kernel(GemmArgs g, Epi epi) {
                     // per wave over 3 stages leave 4, which take the conditional steps)
                     if (c1 - base <= D) {
 #pragma unroll
-                        for (int s = 0; s < D; ++s)
+                        for (int s = 0; s < D; ++s) {
                             if (base + s < c1) compute(s, s % DX);
+                            // shallower activation stages keep streaming (slot s % DX is free)
+                            if constexpr (DX < D) {
+                                if (base + s + DX < c1) loadx(s % DX, base + s + DX);
+                            }
+                        }
                         base = c1;
                     }
                 }
@@ -375,11 +446,12 @@ gemm_kernel(GemmArgs g, Epi epi) {
         const int nt0 = (bx * NWn + q) * g.tpg;
         const int nf = max(0, min(g.tpg, g.n_tiles - nt0));
         if (nf == 0) break;
-        if (g.wscale != nullptr || g.bias != nullptr) {
+        if (g.wscale != nullptr || g.bias != nullptr || g.ssq != nullptr) {
             for (int idx = threadIdx.x; idx < 16 * nf * MR; idx += blockDim.x) {
                 const int n = idx / MR, m = idx % MR;
                 float y = Y[q][n * LDY + m];
                 if (g.wscale != nullptr) y *= g.wscale[nt0 * 16 + n];
+                if (g.ssq != nullptr) y *= rs_sm[m];
                 if (g.bias != nullptr) y += g.bias[nt0 * 16 + n];
                 Y[q][n * LDY + m] = y;
             }
@@ -585,6 +657,56 @@ struct EpiPartial {
             const int qd = idx % nq, ml = idx / nq;
             const float* y = Y + (4 * qd) * ldy + ml;
             *(float4*)(base + (size_t)(m0 + ml) * ldn + n0 + 4 * qd) = make_float4(y[0], y[ldy], y[2 * ldy], y[3 * ldy]);
+        }
+    }
+};
+
+// Residual projection over the whole K range (O or down, one 16-row tile per group):
+// x[m][n] += Y[n][m] for the group's columns n of the real tokens, then the next
+// GEMM's operand u = x * g_next into its fragments and the group's partial sum of
+// x^2 per token, ssq[m][grp] (the consumer folds the partials into its RMSNorm
+// scale).  Padding tokens get u = 0 and a zero partial.  With `slot` (the last layer
+// before a selective LM head) token m's operand and partial go to row slot[m], and
+// tokens without a slot write neither.  Each thread takes four
+// consecutive columns of one token; the four threads of a token sum their squares by
+// a fixed shuffle tree.
+template <bool XF32>
+struct EpiResidual {
+    float* x;               // residual [rows][d]
+    int d, M;
+    const float* g;         // gain of the next RMSNorm [d]
+    void* xg;               // next GEMM's operand fragments (K = d)
+    int KCx;
+    float* ssq;             // [rows][ssq_ld]: partial of row tile grp at [m * ssq_ld + grp]
+    int ssq_ld;
+    const int* slot = nullptr;   // operand / partial row of token m (LM-head slots), or identity
+
+    static constexpr int kSmem = 0;
+    struct Pre {};
+    __device__ void fetch(Pre&, int, int, int, int) const {}
+    __device__ void stage(const Pre&, char*, int, int, int, int) const {}
+
+    __device__ void operator()(float* Y, int ldy, int n0, int nrows, int m0, int mcols, int grp, char*) const {
+        // nrows is 16 (one row tile): 4 quads per token, consecutive threads
+        for (int idx = threadIdx.x; idx < 4 * mcols; idx += blockDim.x) {
+            const int qd = idx & 3, ml = idx >> 2;
+            const int m = m0 + ml, n = n0 + 4 * qd;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f), u = v;
+            if (m < M && n < d) {
+                float4* xp = (float4*)(x + (size_t)m * d + n);
+                v = *xp;
+                const float* y = Y + (4 * qd) * ldy + ml;
+                v.x += y[0]; v.y += y[ldy]; v.z += y[2 * ldy]; v.w += y[3 * ldy];
+                *xp = v;
+                const float4 gg = *(const float4*)(g + n);
+                u = make_float4(v.x * gg.x, v.y * gg.y, v.z * gg.z, v.w * gg.w);
+            }
+            const int dst = slot != nullptr ? (m < M ? slot[m] : -1) : m;
+            if (n < d && dst >= 0) xfrag_store4<XF32>(xg, dst, n, KCx, u);
+            float sq = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+            sq += __shfl_xor(sq, 1);
+            sq += __shfl_xor(sq, 2);
+            if (qd == 0 && dst >= 0) ssq[(size_t)dst * ssq_ld + grp] = sq;
         }
     }
 };

@@ -24,16 +24,20 @@ __device__ __forceinline__ float block_sum(float v, float* red /* NT/64 */) {
     return s;
 }
 
+// With ssq != nullptr (RMSNorm folded into the consumer GEMM) the operand is x * g,
+// not normalised, and the row's sum of x^2 goes to *ssq for the consumer.
 template <bool XF32, int NT, int VPT>
 __device__ __forceinline__ void write_norm_operand(const float4 (&xv)[VPT], int m, int d, float eps, const float* g,
-                                                   void* xg, int KCx, float* red) {
+                                                   void* xg, int KCx, float* red, float* ssq = nullptr) {
     float sq = 0.f;
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
         const int n = 4 * (threadIdx.x + j * NT);
         if (n < d) sq += xv[j].x * xv[j].x + xv[j].y * xv[j].y + xv[j].z * xv[j].z + xv[j].w * xv[j].w;
     }
-    const float rs = 1.0f / sqrtf(block_sum<NT>(sq, red) / d + eps);
+    const float tot = block_sum<NT>(sq, red);
+    if (ssq != nullptr && threadIdx.x == 0) *ssq = tot;
+    const float rs = ssq != nullptr ? 1.0f : 1.0f / sqrtf(tot / d + eps);
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
         const int n = 4 * (threadIdx.x + j * NT);
@@ -49,14 +53,35 @@ __device__ __forceinline__ void write_norm_operand(const float4 (&xv)[VPT], int 
 constexpr int ROW_NT = 1024;
 constexpr int ROW_VPT = 2;      // d up to 8192
 
+// Row selection of the LM head (selective logits skipping): row m of M is kept if
+// it is flagged (need[m] != 0; every row when need is NULL) and fewer than n_sel
+// flagged rows precede it; a kept row's slot is that count.  Returns -1 for a row
+// that is not kept.  Every thread of the block gets the same answer.
+template <int NT>
+__device__ __forceinline__ int lm_slot(const uint8_t* need, int n_sel, int M, int m, float* red) {
+    if (need == nullptr) return (m < M && m < n_sel) ? m : -1;
+    float c = 0.f;
+    for (int i = threadIdx.x; i < m && i < M; i += NT) c += need[i] ? 1.f : 0.f;
+    const int before = (int)block_sum<NT>(c, red);
+    return (m < M && need[m] && before < n_sel) ? before : -1;
+}
+
 // Embedding gather: x[m] = E[id_m] (the MASK id where the mask flag is set) and
-// the first layer's normalised operand.  Padding rows get zeros.
+// the first layer's normalised operand (or, with ssq, the operand x * g and the
+// row's sum of x^2 for an RMSNorm folded into the QKV GEMM).  Padding rows get zeros.
+// With slot != nullptr it also records the row's LM-head slot (lm_slot over need /
+// n_sel) for the last residual projection, which writes the final operand there.
 template <typename ET, bool XF32>
 __global__ void __launch_bounds__(ROW_NT)
 embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int V, int mask_id, float eps,
-             const float* g, float* x, void* xg, int KCx) {
+             const float* g, float* x, void* xg, int KCx, float* ssq, int ssq_ld, int* slot, const uint8_t* need,
+             int n_sel) {
     __shared__ float red[ROW_NT / 64];
     const int m = blockIdx.x;
+    if (slot != nullptr) {
+        const int sl = lm_slot<ROW_NT>(need, n_sel, M, m, red);
+        if (threadIdx.x == 0) slot[m] = sl;
+    }
     float4 xv[ROW_VPT];
     int id = -1;
     if (m < M) {
@@ -74,20 +99,8 @@ embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int
         xv[j] = v;
         if (n < d) *(float4*)(x + (size_t)m * d + n) = v;
     }
-    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red);
-}
-
-// Row selection of the LM head (selective logits skipping): row m of M is kept if
-// it is flagged (need[m] != 0; every row when need is NULL) and fewer than n_sel
-// flagged rows precede it; a kept row's slot is that count.  Returns -1 for a row
-// that is not kept.  Every thread of the block gets the same answer.
-template <int NT>
-__device__ __forceinline__ int lm_slot(const uint8_t* need, int n_sel, int M, int m, float* red) {
-    if (need == nullptr) return (m < M && m < n_sel) ? m : -1;
-    float c = 0.f;
-    for (int i = threadIdx.x; i < m && i < M; i += NT) c += need[i] ? 1.f : 0.f;
-    const int before = (int)block_sum<NT>(c, red);
-    return (m < M && need[m] && before < n_sel) ? before : -1;
+    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red,
+                                              ssq != nullptr ? ssq + (size_t)m * ssq_ld : nullptr);
 }
 
 // Split-K reduction of a residual projection (O or down), one workgroup per row:
