@@ -52,15 +52,13 @@ PREFILL = {"llada8b_bf16_prefill512": ("bf16", 512), "llada8b_bf16_prefill4096":
 MFMA_PEAK_TFLOPS = 2500.0        # bf16 dense
 
 
-def run_e2e(args, dl, torch, shape, dev):
+def e2e_latency(dl, torch, shape, dev, model, repeats=3):
     """Prompt 512 ids; 4 blocks of 32 decoded left to right, 32 denoising steps per
     block with one commit each; after each block: append it to the prefix and
     refresh 4 seeded positions of it with seeded new ids.  Wall-clock latency of the
-    whole generation (prefill included), after one untimed warmup generation."""
+    whole generation (prefill included): (best, all) over `repeats` generations after
+    one untimed warmup generation."""
     P0, B, S, R = 512, shape.block, 32, 4
-    glob = synth.global_weights(shape, "bf16")
-    model = dl.Model(shape, "bf16", glob, lambda l: synth.layer_weights(shape, l, "bf16"), max_window=64,
-                     max_pos=P0 + 4 * B + 64)
     kv = dl.KVCache(model, P0 + 4 * B)
     prompt = torch.from_numpy(synth.prompt_ids(shape, P0)).to(dev)
     picks = [synth.refresh_picks(shape, P0 + b * B, B, R, call=b) for b in range(4)]
@@ -92,14 +90,23 @@ def run_e2e(args, dl, torch, shape, dev):
 
     generate()                                  # warmup (untimed)
     times = []
-    for _ in range(3):
+    for _ in range(repeats):
         fresh_kv()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         generate()
         times.append(time.perf_counter() - t0)
-    lat = min(times)
     kv.close()
+    return min(times), times
+
+
+def run_e2e(args, dl, torch, shape, dev):
+    """End-to-end 128-token generation (e2e_latency) as its own bench line."""
+    P0, B, S, R = 512, shape.block, 32, 4
+    glob = synth.global_weights(shape, "bf16")
+    model = dl.Model(shape, "bf16", glob, lambda l: synth.layer_weights(shape, l, "bf16"), max_window=64,
+                     max_pos=P0 + 4 * B + 64)
+    lat, times = e2e_latency(dl, torch, shape, dev, model)
     model.close()
     return {
         "metric": "end-to-end 128-token generation latency, LLaDA-8B shape, block 32",
@@ -451,6 +458,53 @@ def run_sweep(args, dl, torch, shape, dev):
             "config": {"workload": "llada8b_bf16_p512_msweep", "prefix": P}, "sweep": rows}
 
 
+def tiny_times(dl, torch, dev):
+    """The tiny fp32 model (2 layers, d 256, vocab 1024): prompt 64 ids prefilled, one
+    32-row all-MASK block generated in 4 steps of 8 commits.  Absolute times: one step
+    (dllm_denoise_step + dllm_commit, GPU events over 200 steps at the block's first
+    step) and one whole generation (prefill + 4 steps, wall clock, best of 20)."""
+    sh = synth.TINY
+    w = synth.all_weights(sh, "f32", 0)
+    model = dl.Model(sh, "f32", {k: w[k] for k in ("embed", "lm_head", "final_norm")}, lambda l: w["layers"][l],
+                     max_window=64, max_pos=256)
+    prompt = torch.from_numpy(synth.prompt_ids(sh, 64)).to(dev)
+    tok0, mask0 = synth.window(sh, 32, range(32))
+    d_tok0, d_mask0 = torch.from_numpy(tok0).to(dev), torch.from_numpy(mask0).to(dev)
+    ids = torch.empty(32, dtype=torch.int32, device=dev)
+    conf = torch.empty(32, device=dev)
+    kv = dl.KVCache(model, 96)
+    dl.dllm_prefill(model.handle, kv.handle, prompt, 64)
+    tok, mask = d_tok0.clone(), d_mask0.clone()
+    for _ in range(10):
+        dl.dllm_denoise_step(model.handle, kv.handle, d_tok0, d_mask0, 32, ids, conf)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = 200
+    e0.record()
+    for _ in range(n):
+        dl.dllm_denoise_step(model.handle, kv.handle, d_tok0, d_mask0, 32, ids, conf)
+        dl.dllm_commit(conf, ids, tok, mask, 0, 32, 8)
+    e1.record()
+    torch.cuda.synchronize()
+    step_ms = e0.elapsed_time(e1) / n
+    kv.close()
+    gens = []
+    for _ in range(21):
+        kv = dl.KVCache(model, 96)
+        tok, mask = d_tok0.clone(), d_mask0.clone()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        dl.dllm_prefill(model.handle, kv.handle, prompt, 64)
+        for _ in range(4):
+            dl.dllm_denoise_step(model.handle, kv.handle, tok, mask, 32, ids, conf)
+            dl.dllm_commit(conf, ids, tok, mask, 0, 32, 8)
+        torch.cuda.synchronize()
+        gens.append(time.perf_counter() - t0)
+        kv.close()
+    model.close()
+    return {"workload": "tiny fp32: 2 layers, d 256, prompt 64, one 32-row block in 4 steps of 8 commits",
+            "step_ms": round(step_ms, 4), "generation_ms": round(1e3 * min(gens[1:]), 3)}
+
+
 def measured_read_peak(dl, torch, dev, gib=4):
     """Streaming-read rate of the library's plain read kernel over `gib` GiB (best of 5 launches)."""
     buf = torch.empty(gib << 30, dtype=torch.uint8, device=dev)
@@ -584,8 +638,11 @@ def main():
 
     t0 = time.time()
     glob = synth.global_weights(shape, "bf16")
+    # the default workload's model also serves the end-to-end generation (prompt 512 +
+    # 128 tokens) and the down-projection M-sweep (windows up to 256 rows)
+    extras = args.workload == DEFAULT
     model = dl.Model(shape, dtype, glob, lambda l: synth.layer_weights(shape, l, "bf16"),
-                     max_window=64, max_pos=P + W + 64)
+                     max_window=256 if extras else 64, max_pos=max(P + W + 64, 1024 if extras else 0))
     log(f"model created in {time.time() - t0:.1f} s")
     kv = dl.KVCache(model, P + W)
     prompt = synth.prompt_ids(shape, P)
@@ -701,6 +758,32 @@ def main():
                     for k, v in kern.items()},
         "roofline": roof,
     }
+    # the dispatch gap: step time minus the per-class replay time of its launches (the
+    # replays include each launch's own ramp and drain; the gap holds the embedding, the
+    # LM-head merge, the commit and the switches between kernels)
+    class_ms = sum(v["launches_per_step"] * v["mean_us"] for v in kern.values()) / 1e3
+    out["dispatch_gap_ms"] = round(ms - class_ms, 4)
+    out["sum_of_class_replays_ms"] = round(class_ms, 4)
+    if extras:
+        # down projection alone (GEMM + its residual reduction) against the window's rows:
+        # latency stays flat while the weight stream dominates
+        kv_s = dl.KVCache(model, 256)
+        sweep = []
+        for Ws in (1, 2, 4, 8, 16, 32, 64, 128, 256):
+            dl.dllm_kernel_replay(model.handle, kv_s.handle, dl.K_DOWN, Ws, shape.n_layers)
+            r0.record()
+            dl.dllm_kernel_replay(model.handle, kv_s.handle, dl.K_DOWN, Ws, 2 * shape.n_layers)
+            r1.record()
+            torch.cuda.synchronize()
+            sweep.append([Ws, round(r0.elapsed_time(r1) * 1e3 / (2 * shape.n_layers), 2)])
+        kv_s.close()
+        out["down_proj_msweep_us"] = sweep
+        lat, lats = e2e_latency(dl, torch, shape, dev, model, repeats=2)
+        out["e2e128"] = {"workload": "llada8b_bf16_e2e128: prompt 512, 4 blocks x 32 steps (1 commit each), "
+                                     "append + 4-row refresh per block", "latency_s": round(lat, 4),
+                         "tokens_s": round(128 / lat, 2), "latencies_s": [round(t, 4) for t in lats]}
+        out["tiny_fp32"] = tiny_times(dl, torch, dev)
+        log(f"e2e {lat:.3f} s; tiny {out['tiny_fp32']}")
     if not args.no_cpu_baseline:
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(shape, dtype, wl, prompt, tok, mask, glob)

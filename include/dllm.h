@@ -64,7 +64,7 @@ extern "C" {
 
 /* Weight / arithmetic types. */
 #define DLLM_F32 0   /* fp32 weights, fp32 activations and KV cache */
-#define DLLM_BF16 1  /* bf16 weights; activations, Q and the KV cache as bf16 hi/lo pairs; fp32 accumulate */
+#define DLLM_BF16 1  /* bf16 weights; GEMM activations as bf16 hi/lo pairs, Q as fp16 hi/lo, KV cache fp16; fp32 accumulate */
 #define DLLM_W8 2    /* int8 weights with fp32 per-output-row scales; activations as for DLLM_BF16 */
 #define DLLM_Q4 3    /* Q4_0 weights (see dllm_quantize_q4_0); activations as for DLLM_BF16 */
 
@@ -139,17 +139,14 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
 int dllm_model_destroy(dllm_model* m);
 
 /* Bytes of device memory a KV cache of `capacity` positions needs (4 bytes per
- * cached value).  Layout inside the caller's buffer, with Cs = capacity rounded
- * up to a multiple of 32, H = n_kv_heads (n_heads if 0) and P = H*Cs*Dh elements
- * per plane:
- *   F32 models, element float, 2 planes per layer (K, V^T):
+ * cached value for DLLM_F32 models, 2 otherwise).  Layout inside the caller's
+ * buffer, with Cs = capacity rounded up to a multiple of 32, H = n_kv_heads (n_heads
+ * if 0) and P = H*Cs*Dh elements per plane, 2 planes per layer (K, V^T):
  *     K   of layer l, head h, position p, dim j: (l*2+0)*P + (h*Cs + p)*Dh + j
  *     V^T of layer l, head h, dim j, position p: (l*2+1)*P + (h*Dh + j)*Cs + p
- *   BF16 / W8 models, element bfloat16, 4 planes per layer (K hi, K lo, V^T hi,
- *   V^T lo); a value is hi + lo with hi = bf16(v), lo = bf16(v - hi):
- *     K   hi / lo: (l*4+0)*P + ... / (l*4+1)*P + ...   (same offsets as above)
- *     V^T hi / lo: (l*4+2)*P + ... / (l*4+3)*P + ...
- * K is stored after RoPE. */
+ * Elements are float for DLLM_F32 models and IEEE fp16 (round to nearest even,
+ * saturated at +-65504) for DLLM_BF16, DLLM_W8 and DLLM_Q4 models.  K is stored after
+ * RoPE. */
 int dllm_kv_bytes(const dllm_model* m, int32_t capacity, size_t* bytes);
 
 /* Wraps a caller-owned device buffer of at least dllm_kv_bytes() bytes as a KV
@@ -334,8 +331,10 @@ int dllm_kernel_replay(dllm_model* m, dllm_kv* kv, int32_t kernel_class, int32_t
                        dllm_stream stream);
 
 /* Algorithmic bytes one launch of a kernel class moves for a window of W rows at
- * prefix P (weights once, KV read, KV written, activations; no logits).  Used to
- * express achieved bandwidth. */
+ * prefix P: every weight once (with int8 row scales, Q4_0 block scales, Q/K/V
+ * biases), the K/V the attention reads and the K/V rows QKV writes, one value per
+ * element (4 bytes for DLLM_F32 models, 2 otherwise); no activations (L2-resident) and
+ * no logits.  Used to express achieved bandwidth against the HBM roofline. */
 int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes);
 
 /* Token states of staged stabilisation (one byte per window position). */

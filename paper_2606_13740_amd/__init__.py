@@ -361,8 +361,8 @@ class KVCache:
     def views(self):
         """(K [L][Hkv][Cs][Dh], V^T [L][Hkv][Dh][Cs]) as float32 tensors (Hkv K/V heads).
 
-        fp32 models: views of the buffer.  bf16 / int8 models: hi + lo of the two
-        bf16 planes (a new tensor, not a view)."""
+        fp32 models: views of the buffer.  bf16 / int8 / Q4_0 models: the fp16 planes,
+        widened (a new tensor, not a view)."""
         import torch
 
         sh = self.model.shape
@@ -374,9 +374,9 @@ class KVCache:
             per = flat.view(sh.n_layers, 2, plane)
             K, Vt = per[:, 0], per[:, 1]
         else:
-            flat = self.buf.view(torch.uint8)[: sh.n_layers * 4 * plane * 2].view(torch.bfloat16)
-            per = flat.view(sh.n_layers, 4, plane).float()
-            K, Vt = per[:, 0] + per[:, 1], per[:, 2] + per[:, 3]
+            flat = self.buf.view(torch.uint8)[: sh.n_layers * 2 * plane * 2].view(torch.float16)
+            per = flat.view(sh.n_layers, 2, plane).float()
+            K, Vt = per[:, 0], per[:, 1]
         return (K.reshape(sh.n_layers, Hkv, Cs, sh.head_dim),
                 Vt.reshape(sh.n_layers, Hkv, sh.head_dim, Cs))
 

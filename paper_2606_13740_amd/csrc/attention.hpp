@@ -20,10 +20,9 @@ namespace dllm {
 
 struct AttnArgs {
     const void* q;        // [rows][H][Dh]
-    size_t q_plane;       // elements from the hi to the lo plane of q (bf16 path)
+    size_t q_plane;       // elements from the hi to the lo plane of q (fp16 path)
     const void* K;        // layer base [Hkv][Cs][Dh]
     const void* Vt;       // layer base [Hkv][Dh][Cs]
-    size_t kv_plane;      // elements from the hi to the lo plane of K and V^T (bf16 path)
     int Cs;               // cache row stride (multiple of 32)
     int H;                // query heads
     int G;                // query heads per K/V head (grouped-query attention; 1 = multi-head)
@@ -39,9 +38,10 @@ struct AttnArgs {
     int rows_ld;
 };
 
-// bf16 MFMA path.  Q, K and V are carried as hi + lo bf16 planes and each
-// product takes three MFMAs (hi*hi + hi*lo + lo*hi), so scores and outputs keep
-// ~16 significant bits; the probabilities P are split the same way.
+// fp16 MFMA path (v_mfma_f32_16x16x32_f16).  The cache holds K and V^T as one fp16
+// plane each; Q arrives as an fp16 hi + lo pair and the probabilities P are split the
+// same way in registers, so every product takes two MFMAs (K * Q_hi + K * Q_lo,
+// V^T * P_hi + V^T * P_lo) and the scores and outputs keep the cache's precision.
 //
 // Workgroup = (key split, head, group of QG query tiles of 16 rows), one wave per
 // query tile.  The split's 32-key blocks are staged in LDS once per workgroup
@@ -49,8 +49,8 @@ struct AttnArgs {
 // next block streams in while the current one is used, and every wave reads its
 // MFMA fragments from LDS.  LDS rows are XOR-swizzled in 16-byte columns so that
 // the 16 rows one fragment read touches fall in distinct banks:
-//   K plane  [32 keys][Dh/8 cols]: col' = col ^ (((key & 3) | (4 * ((key >> 3) & 3))) mod Dh/8)
-//   V^T plane [Dh dims][4 cols]:   col' = col ^ ((dim >> 2) & 3)
+//   K  [32 keys][Dh/8 cols]: col' = col ^ (((key & 3) | (4 * ((key >> 3) & 3))) mod Dh/8)
+//   V^T [Dh dims][4 cols]:   col' = col ^ ((dim >> 2) & 3)
 // With one split the normalised output goes to the O projection's fragments;
 // otherwise (m, l, o) per split goes to attn_combine.
 __device__ __forceinline__ int swz_k(int key) { return (key & 3) | (((key >> 3) & 3) << 2); }
@@ -58,13 +58,13 @@ __device__ __forceinline__ int swz_k(int key) { return (key & 3) | (((key >> 3) 
 typedef __attribute__((address_space(3))) void lds_void;
 
 template <int DH, int QG>
-__global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
     constexpr int NC = DH / 32;               // 32-dim chunks
     constexpr int ND = DH / 16;               // 16-dim output tiles
     constexpr int KCOLS = DH / 8;             // 16-byte columns per key row
-    constexpr int KPLANE = 32 * DH * 2;       // bytes of one K plane of a block
-    constexpr int VPLANE = DH * 64;           // bytes of one V^T plane of a block
-    constexpr int BUF = 2 * KPLANE + 2 * VPLANE;
+    constexpr int KPLANE = 32 * DH * 2;       // bytes of a block's K (fp16)
+    constexpr int VPLANE = DH * 64;           // bytes of a block's V^T (fp16)
+    constexpr int BUF = KPLANE + VPLANE;
     constexpr int NSLOT = BUF / 16;           // 16-byte slots per block
     static_assert(NSLOT % 64 == 0, "block must be whole wave loads");
     __shared__ __attribute__((aligned(1024))) char lds[2 * BUF];
@@ -94,17 +94,15 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
             if (i >= NSLOT / 64) break;
             const int sl = i * 64 + lane;
             const uint16_t* src;
-            if (sl < KPLANE / 8) {                       // K: two planes of 32 x KCOLS slots
-                const int pl = sl / (KPLANE / 16), s2 = sl % (KPLANE / 16);
-                const int key = s2 / KCOLS, pc = s2 % KCOLS;
+            if (sl < KPLANE / 16) {                      // K: 32 x KCOLS slots
+                const int key = sl / KCOLS, pc = sl % KCOLS;
                 const int col = pc ^ (swz_k(key) & (KCOLS - 1));
-                src = Kp + pl * a.kv_plane + (size_t)(k0 + key) * DH + col * 8;
-            } else {                                     // V^T: two planes of DH x 4 slots
-                const int s1 = sl - KPLANE / 8;
-                const int pl = s1 / (VPLANE / 16), s2 = s1 % (VPLANE / 16);
-                const int dim = s2 >> 2, pc = s2 & 3;
+                src = Kp + (size_t)(k0 + key) * DH + col * 8;
+            } else {                                     // V^T: DH x 4 slots
+                const int s1 = sl - KPLANE / 16;
+                const int dim = s1 >> 2, pc = s1 & 3;
                 const int col = pc ^ ((dim >> 2) & 3);
-                src = Vp + pl * a.kv_plane + (size_t)dim * a.Cs + k0 + col * 8;
+                src = Vp + (size_t)dim * a.Cs + k0 + col * 8;
             }
             __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(base + i * 1024), 16, 0, 0);
         }
@@ -133,7 +131,7 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
         __syncthreads();                        // ... and everyone's; `cur ^ 1` is free again
         if (kb + 1 < kb1) stage(kb + 1, cur ^ 1);
         const char* Kb = lds + cur * BUF;
-        const char* Vb = Kb + 2 * KPLANE;
+        const char* Vb = Kb + KPLANE;
         const int k0 = kb * 32;
 
         f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -143,12 +141,10 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
             for (int t = 0; t < 2; ++t) {
                 const int key = krow0 + 4 * t;
                 const int off = key * (DH * 2) + (((4 * c + g) ^ (swz_k(key) & (KCOLS - 1))) << 4);
-                const u32x4_t kh = *(const u32x4_t*)(Kb + off);
-                const u32x4_t kl = *(const u32x4_t*)(Kb + KPLANE + off);
+                const u32x4_t kf = *(const u32x4_t*)(Kb + off);
                 f32x4_t& sa = t ? s1 : s0;
-                sa = mfma_bf16(kh, qf[c][0], sa);
-                sa = mfma_bf16(kh, qf[c][1], sa);
-                sa = mfma_bf16(kl, qf[c][0], sa);
+                sa = mfma_f16(kf, qf[c][0], sa);
+                sa = mfma_f16(kf, qf[c][1], sa);
             }
         }
 
@@ -173,12 +169,11 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
             for (int e = 0; e < 4; ++e) {
                 const float p0 = exp2f(sv[2 * e] - mnew), p1 = exp2f(sv[2 * e + 1] - mnew);
                 ps += p0 + p1;
-                // p in [0, 1]: hi = truncation, lo = the rounded remainder
-                const uint32_t u0 = __float_as_uint(p0), u1 = __float_as_uint(p1);
-                const float r0 = p0 - __uint_as_float(u0 & 0xFFFF0000u);
-                const float r1 = p1 - __uint_as_float(u1 & 0xFFFF0000u);
-                phi[e] = (u0 >> 16) | (u1 & 0xFFFF0000u);
-                plo[e] = (uint32_t)f32_to_bf16(r0) | ((uint32_t)f32_to_bf16(r1) << 16);
+                // p in [0, 1]: hi = fp16 toward zero, lo = the remainder toward zero
+                const auto h = __builtin_amdgcn_cvt_pkrtz(p0, p1);
+                const auto l = __builtin_amdgcn_cvt_pkrtz(p0 - (float)h[0], p1 - (float)h[1]);
+                phi[e] = __builtin_bit_cast(uint32_t, h);
+                plo[e] = __builtin_bit_cast(uint32_t, l);
             }
         }
         lrun = lrun * alpha + ps;
@@ -192,20 +187,17 @@ __global__ void __launch_bounds__(QG * 64) attn_bf16_kernel(AttnArgs a) {
             for (int i = 0; i < 4; ++i) oacc[dt][i] *= alpha;
             const int dim = 16 * dt + r;
             const int off = dim * 64 + ((g ^ ((dim >> 2) & 3)) << 4);
-            u32x4_t vh = *(const u32x4_t*)(Vb + off);
-            u32x4_t vl = *(const u32x4_t*)(Vb + VPLANE + off);
+            u32x4_t vf = *(const u32x4_t*)(Vb + off);
             if (tail) {                          // zero V beyond T (those rows may be unwritten)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int key = k0 + 8 * g + 2 * e;
                     const uint32_t keep = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
-                    vh[e] &= keep;
-                    vl[e] &= keep;
+                    vf[e] &= keep;
                 }
             }
-            oacc[dt] = mfma_bf16(vh, ph, oacc[dt]);
-            oacc[dt] = mfma_bf16(vh, pl, oacc[dt]);
-            oacc[dt] = mfma_bf16(vl, ph, oacc[dt]);
+            oacc[dt] = mfma_f16(vf, ph, oacc[dt]);
+            oacc[dt] = mfma_f16(vf, pl, oacc[dt]);
         }
     }
 

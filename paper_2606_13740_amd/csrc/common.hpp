@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
@@ -125,6 +126,12 @@ __device__ __forceinline__ f32x4_t mfma_bf16(const u32x4_t& a, const u32x4_t& b,
                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
+// v_mfma_f32_16x16x32_f16: the same operand layout with fp16 elements.
+__device__ __forceinline__ f32x4_t mfma_f16(const u32x4_t& a, const u32x4_t& b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
+                                                 0, 0, 0);
+}
+
 __device__ __forceinline__ f32x4_t mfma_f32(float a, float b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
@@ -162,6 +169,17 @@ __device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
 
 __device__ __forceinline__ uint16_t f32_to_f16_bits(float f) {
     return __builtin_bit_cast(uint16_t, (_Float16)f);    // round to nearest even
+}
+
+// fp16 cache values: round to nearest even, saturated to the largest finite fp16.
+__device__ __forceinline__ uint16_t f16_sat(float v) { return f32_to_f16_bits(fminf(fmaxf(v, -65504.f), 65504.f)); }
+
+// hi / lo fp16 split (an fp16 MFMA operand with ~21 significant bits): hi = fp16(v),
+// lo = fp16(v - hi), both saturated.
+__device__ __forceinline__ void split_f16(float v, uint16_t& hi, uint16_t& lo) {
+    v = fminf(fmaxf(v, -65504.f), 65504.f);
+    hi = f32_to_f16_bits(v);
+    lo = f32_to_f16_bits(v - f16_bits_to_f32(hi));
 }
 
 // Q4_0 decision for one block of 32 columns [k0, k0 + 32) of a row (columns >= K

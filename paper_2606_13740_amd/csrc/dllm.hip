@@ -101,7 +101,7 @@ struct dllm_model {
     dllm_config cfg;
     int wt = 0;              // WT_F32 / WT_BF16 / WT_I8
     bool xf32 = false;       // activations in fp32
-    size_t kv_elem = 4;      // bytes per cached K or V value (fp32, or a bf16 hi/lo pair)
+    size_t kv_elem = 4;      // bytes per cached K or V value (fp32 or fp16)
     int KCx_d = 0, KCx_f = 0;
     int Hkv = 0, dkv = 0;    // K/V heads and K (or V) rows per layer
     std::vector<LayerW> layers;
@@ -617,25 +617,23 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                            m->KCx_d, fused ? w.ssq : nullptr, w.ssq_ld, (fused && lm_sel_last) ? w.slot : nullptr, a.need,
                            a.n_sel);
 
-    // Cache per layer: fp32 [K][V^T], or bf16 [K hi][K lo][V^T hi][V^T lo]; Hkv heads.
+    // Cache per layer: [K][V^T], fp32 or fp16; Hkv heads.  Q: fp32, or fp16 hi / lo planes.
     const size_t plane = (size_t)m->Hkv * kv->Cs * Dh;
-    const size_t layer_elems = (XF32 ? 2 : 4) * plane;
-    const size_t kv_plane = XF32 ? 0 : plane;
+    const size_t layer_elems = 2 * plane;
     const size_t q_plane = XF32 ? 0 : (size_t)w.rows * d;
     const int n_iter = a.replay < 0 ? a.n_layers : (a.replay == DLLM_K_LMHEAD ? 0 : a.n_replay);
     for (int it = 0; it < n_iter; ++it) {
         const int l = it % c.n_layers;
         LayerW& L = m->layers[l];
         AT* Kc = (AT*)kv->buf + (size_t)l * layer_elems;
-        AT* Vt = Kc + (XF32 ? plane : 2 * plane);
+        AT* Vt = Kc + plane;
 
         // RMSNorm + QKV + RoPE -> Q buffer and K/V cache rows
         if (run(DLLM_K_QKV)) {
             GemmArgs g{L.qkv.w, L.qkv.scale, w.xg, L.qkv.KCw, L.qkv.KCw * WTraits<WT>::XPER, L.qkv.n_tiles, L.bqkv};
             g.qs = L.qkv.qs;
             if (fused && (l == 0 || FUSE_DOWN)) fold_norm(g, m, w, nssq_qkv(l));
-            EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv_plane,
-                           kv->Cs};
+            EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv->Cs};
             ProbeScope ps(m, DLLM_K_QKV, s);
             if ((rc = launch_gemm<WT, G_QKV>(decomp(G_QKV, WT, L.qkv.n_tiles, Mc, gy), L.qkv.n_tiles, MT, g, e, gy, s)))
                 return rc;
@@ -643,7 +641,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
         // attention over [0, T) (+ split merge)
         if (run(DLLM_K_ATTN)) {
             AttnArgs at{};
-            at.q = w.q; at.q_plane = q_plane; at.K = Kc; at.Vt = Vt; at.kv_plane = kv_plane; at.Cs = kv->Cs; at.H = H;
+            at.q = w.q; at.q_plane = q_plane; at.K = Kc; at.Vt = Vt; at.Cs = kv->Cs; at.H = H;
             at.G = H / m->Hkv; at.T = a.T; at.lim = a.lim; at.M = a.M;
             at.scale = 1.0f / sqrtf((float)Dh); at.o = w.of; at.KCx = m->KCx_d;
             at.opart = w.opart; at.mlpart = w.mlpart; at.rows_ld = w.wrows;
@@ -670,7 +668,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
                 dim3 grid(at.nsplit, H, nqg);
-#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_bf16_kernel<DH_, QG_>), grid, dim3(QG_ * 64), 0, s, at)
+#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_>), grid, dim3(QG_ * 64), 0, s, at)
 #define ATTN_QG(DH_) \
     do { if (QG == 8) ATTN(DH_, 8); else if (QG == 4) ATTN(DH_, 4); else if (QG == 3) ATTN(DH_, 3); \
          else if (QG == 2) ATTN(DH_, 2); \
@@ -829,7 +827,7 @@ int dllm_model_create(const dllm_config* cfg, const dllm_weights* w, dllm_stream
     const dllm_config& c = m->cfg;
     m->wt = c.dtype == DLLM_F32 ? WT_F32 : (c.dtype == DLLM_BF16 ? WT_BF16 : (c.dtype == DLLM_W8 ? WT_I8 : WT_Q4));
     m->xf32 = c.dtype == DLLM_F32;
-    m->kv_elem = 4;
+    m->kv_elem = m->xf32 ? 4 : 2;
     m->Hkv = c.n_kv_heads > 0 ? c.n_kv_heads : c.n_heads;
     m->dkv = m->Hkv * c.head_dim;
     const int xcols = m->xf32 ? 16 : 32;
@@ -1271,22 +1269,23 @@ int dllm_kernel_replay(dllm_model* m, dllm_kv* kv, int32_t kernel_class, int32_t
 int dllm_kernel_bytes(const dllm_model* m, int32_t kernel_class, int32_t W, int32_t P, double* bytes) {
     if (!m || !bytes) return fail(DLLM_E_INVAL, "NULL argument");
     const dllm_config& c = m->cfg;
-    // bytes per weight (Q4_0: a 4-bit code plus a 2-byte scale per 32 weights)
+    // What the method must move (no logits, no activations: those stay in L2): every
+    // weight once (Q4_0: a 4-bit code plus a 2-byte scale per 32 weights; int8: plus a
+    // 4-byte scale per row; Q/K/V biases), the K/V it reads and the K/V rows it writes
+    // at one value per element (4 bytes for fp32 models, 2 otherwise).
     const double wsz = m->wt == WT_F32 ? 4.0 : (m->wt == WT_BF16 ? 2.0 : (m->wt == WT_I8 ? 1.0 : 0.5 + 2.0 / 32));
-    const double asz = (double)m->kv_elem;   // activations and cache values: 4 bytes
+    const double vsz = m->wt == WT_F32 ? 4.0 : 2.0;
     const double d = c.d_model, F = c.d_ff, V = c.vocab, dkv = m->dkv;
     const double scale_b = (m->wt == WT_I8) ? 4.0 : 0.0;   // per weight row
     const double bias_b = c.qkv_bias ? 4.0 : 0.0;           // per Q/K/V row
     double b = 0;
     switch (kernel_class) {
-        case DLLM_K_QKV:
-            b = (d + 2 * dkv) * (d * wsz + scale_b + bias_b) + W * d * asz + 2.0 * W * dkv * asz + W * d * asz;
-            break;
-        case DLLM_K_ATTN: b = 2.0 * (P + W) * dkv * asz + 2.0 * W * d * asz; break;
-        case DLLM_K_OPROJ: b = d * d * wsz + d * scale_b + W * d * asz + 2.0 * W * d * 4 + W * d * asz; break;
-        case DLLM_K_GATEUP: b = 2 * F * d * wsz + 2 * F * scale_b + W * d * asz + W * F * asz; break;
-        case DLLM_K_DOWN: b = d * F * wsz + d * scale_b + W * F * asz + 2.0 * W * d * 4 + W * d * asz; break;
-        case DLLM_K_LMHEAD: b = V * d * wsz + V * scale_b + W * d * asz; break;
+        case DLLM_K_QKV: b = (d + 2 * dkv) * (d * wsz + scale_b + bias_b) + 2.0 * W * dkv * vsz; break;
+        case DLLM_K_ATTN: b = 2.0 * (P + W) * dkv * vsz; break;
+        case DLLM_K_OPROJ: b = d * d * wsz + d * scale_b; break;
+        case DLLM_K_GATEUP: b = 2 * F * d * wsz + 2 * F * scale_b; break;
+        case DLLM_K_DOWN: b = d * F * wsz + d * scale_b; break;
+        case DLLM_K_LMHEAD: b = V * d * wsz + V * scale_b; break;
         default: return fail(DLLM_E_INVAL, "unknown kernel class");
     }
     *bytes = b;

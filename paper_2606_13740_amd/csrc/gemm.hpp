@@ -469,8 +469,9 @@ gemm_kernel(GemmArgs g, Epi epi) {
 // Q/K/V projection: RoPE on Q and K, Q to a row-major buffer, K and V to the
 // cache at each token's position.  Packed rows: [Q | K | V], each d rows; inside
 // a Q or K head, packed row 2i is dim i and row 2i+1 is dim i + Dh/2, so a RoPE
-// pair is two adjacent rows.  fp32 models store one fp32 plane; bf16 / int8
-// models store a hi and a lo bf16 plane (`plane` elements apart).
+// pair is two adjacent rows.  fp32 models store fp32; bf16 / int8 / Q4_0 models
+// store K and V as one fp16 plane and Q as an fp16 hi and lo plane (`q_plane`
+// elements apart), the operands of the attention's fp16 MFMAs.
 template <bool XF32>
 struct EpiQKV {
     using T = typename std::conditional<XF32, float, uint16_t>::type;
@@ -480,23 +481,27 @@ struct EpiQKV {
     const float2* rope;     // [max_pos][Dh/2] (cos, sin)
     T* q;                   // [rows][d] (+ lo plane at q + q_plane)
     size_t q_plane;
-    T* Kc;                  // layer base of K   [Hkv][Cs][Dh] (+ lo plane at kv_plane)
-    T* Vt;                  // layer base of V^T [Hkv][Dh][Cs] (+ lo plane at kv_plane)
-    size_t kv_plane;
+    T* Kc;                  // layer base of K   [Hkv][Cs][Dh]
+    T* Vt;                  // layer base of V^T [Hkv][Dh][Cs]
     int Cs;
 
     static constexpr int kPairs = 24 * 64;          // staged (cos, sin): 3 row tiles x 64 tokens
     static constexpr int kSmem = kPairs * 8;
 
-    __device__ __forceinline__ static void put(T* p, size_t plane, float v) {
+    // one Q value (fp16 hi and lo planes) / one cache value (one fp16 plane)
+    __device__ __forceinline__ static void put_q(T* p, size_t plane, float v) {
         if constexpr (XF32) {
             *p = v;
         } else {
             uint16_t hi, lo;
-            split_bf16(v, hi, lo);
+            split_f16(v, hi, lo);
             p[0] = hi;
             p[plane] = lo;
         }
+    }
+    __device__ __forceinline__ static void put_kv(T* p, float v) {
+        if constexpr (XF32) *p = v;
+        else *p = f16_sat(v);
     }
 
     // (cos, sin) of every (pair, token) of the group's Q/K rows: the first kPre per
@@ -540,16 +545,25 @@ struct EpiQKV {
         }
     }
 
-    // four consecutive values of one plane pair (fp32: one 16-byte store; bf16: 8-byte hi and lo stores)
-    __device__ __forceinline__ static void put4(T* p, size_t plane, const float (&v)[4]) {
+    // four consecutive Q values (fp32: one 16-byte store; else 8-byte hi and lo stores)
+    __device__ __forceinline__ static void put4_q(T* p, size_t plane, const float (&v)[4]) {
         if constexpr (XF32) {
             *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
         } else {
             uint16_t h[4], l[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) split_bf16(v[e], h[e], l[e]);
+            for (int e = 0; e < 4; ++e) split_f16(v[e], h[e], l[e]);
             *(uint2*)p = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
             *(uint2*)(p + plane) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+        }
+    }
+    // four consecutive cache values (fp32: 16 bytes; else one 8-byte fp16 store)
+    __device__ __forceinline__ static void put4_kv(T* p, const float (&v)[4]) {
+        if constexpr (XF32) {
+            *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+            *(uint2*)p = make_uint2(f16_sat(v[0]) | ((uint32_t)f16_sat(v[1]) << 16),
+                                    f16_sat(v[2]) | ((uint32_t)f16_sat(v[3]) << 16));
         }
     }
 
@@ -577,10 +591,15 @@ struct EpiQKV {
                     ra[e] = a * cs.x - b * cs.y;
                     rb[e] = a * cs.y + b * cs.x;
                 }
-                T* dst = (seg == 0) ? q + (size_t)m * d + h * Dh : Kc + ((size_t)h * Cs + ps) * Dh;
-                const size_t plane = (seg == 0) ? q_plane : kv_plane;
-                put4(dst + j0, plane, ra);
-                put4(dst + j0 + half, plane, rb);
+                if (seg == 0) {
+                    T* dst = q + (size_t)m * d + h * Dh;
+                    put4_q(dst + j0, q_plane, ra);
+                    put4_q(dst + j0 + half, q_plane, rb);
+                } else {
+                    T* dst = Kc + ((size_t)h * Cs + ps) * Dh;
+                    put4_kv(dst + j0, ra);
+                    put4_kv(dst + j0 + half, rb);
+                }
             }
             return;
         }
@@ -598,9 +617,9 @@ struct EpiQKV {
                 const float* y = Y + nl * ldy + 4 * tq;
                 if (m + 3 < M) {
                     const float v[4] = {y[0], y[1], y[2], y[3]};
-                    put4(dst, kv_plane, v);
+                    put4_kv(dst, v);
                 } else {
-                    for (int e = 0; e < 4 && m + e < M; ++e) put(dst + e, kv_plane, y[e]);
+                    for (int e = 0; e < 4 && m + e < M; ++e) put_kv(dst + e, y[e]);
                 }
             }
             return;
@@ -623,17 +642,17 @@ struct EpiQKV {
                 const float rb = a * cs.y + b * cs.x;
                 if (seg == 0) {
                     T* dst = q + (size_t)m * d + h * Dh;
-                    put(dst + j, q_plane, ra);
-                    put(dst + j + half, q_plane, rb);
+                    put_q(dst + j, q_plane, ra);
+                    put_q(dst + j + half, q_plane, rb);
                 } else {
                     T* dst = Kc + ((size_t)h * Cs + ps) * Dh;
-                    put(dst + j, kv_plane, ra);
-                    put(dst + j + half, kv_plane, rb);
+                    put_kv(dst + j, ra);
+                    put_kv(dst + j + half, rb);
                 }
             } else {
                 T* dst = Vt + ((size_t)h * Dh + rr) * Cs + ps;
-                put(dst, kv_plane, a);
-                put(dst + Cs, kv_plane, b);
+                put_kv(dst, a);
+                put_kv(dst + Cs, b);
             }
         }
     }
