@@ -43,22 +43,25 @@ struct AttnArgs {
 // same way in registers, so every product takes two MFMAs (K * Q_hi + K * Q_lo,
 // V^T * P_hi + V^T * P_lo) and the scores and outputs keep the cache's precision.
 //
-// Workgroup = (key split, head, group of QG query tiles of 16 rows), one wave per
-// query tile.  The split's 32-key blocks are staged in LDS once per workgroup
-// with direct global->LDS loads (global_load_lds_dwordx4), double-buffered so the
-// next block streams in while the current one is used, and every wave reads its
-// MFMA fragments from LDS.  LDS rows are XOR-swizzled in 16-byte columns so that
+// Workgroup = (key split, head, group of QG query tiles of 16 rows), KS x QG waves:
+// KS key groups of QG waves, one wave per query tile.  Key group k takes the split's
+// 32-key blocks k, k + KS, ...; each block is staged in the group's own LDS buffers
+// once with direct global->LDS loads (global_load_lds_dwordx4), double-buffered so the
+// next block streams in while the current one is used, and the group's waves read
+// their MFMA fragments from LDS.  With KS > 1 the groups' partial (max, sum, O)
+// states are merged in LDS in group order at the end.  LDS rows are XOR-swizzled in 16-byte columns so that
 // the 16 rows one fragment read touches fall in distinct banks:
 //   K  [32 keys][Dh/8 cols]: col' = col ^ (((key & 3) | (4 * ((key >> 3) & 3))) mod Dh/8)
 //   V^T [Dh dims][4 cols]:   col' = col ^ ((dim >> 2) & 3)
 // With one split the normalised output goes to the O projection's fragments;
-// otherwise (m, l, o) per split goes to attn_combine.
+// otherwise (m, l, o) per split goes to attn_combine.  Short key ranges take KS > 1
+// and a single split, which leaves no merge launch.
 __device__ __forceinline__ int swz_k(int key) { return (key & 3) | (((key >> 3) & 3) << 2); }
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int DH, int QG>
-__global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
+template <int DH, int QG, int KS>
+__global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
     constexpr int NC = DH / 32;               // 32-dim chunks
     constexpr int ND = DH / 16;               // 16-dim output tiles
     constexpr int KCOLS = DH / 8;             // 16-byte columns per key row
@@ -67,12 +70,15 @@ __global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
     constexpr int BUF = KPLANE + VPLANE;
     constexpr int NSLOT = BUF / 16;           // 16-byte slots per block
     static_assert(NSLOT % 64 == 0, "block must be whole wave loads");
-    __shared__ __attribute__((aligned(1024))) char lds[2 * BUF];
+    constexpr int MLD = DH + 4;               // merge: floats per (group, row) record
+    constexpr int MERGE = KS > 1 ? KS * QG * 16 * (MLD + 2) * 4 : 0;
+    __shared__ __attribute__((aligned(1024))) char lds[KS * 2 * BUF > MERGE ? KS * 2 * BUF : MERGE];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
+    const int grp = wave / QG, qw = wave % QG;                // key group, query tile
     const int split = blockIdx.x, h = blockIdx.y;
-    const int row = blockIdx.z * 16 * QG + 16 * wave + r;    // this lane's query row
+    const int row = blockIdx.z * 16 * QG + 16 * qw + r;      // this lane's query row
     const int ld = a.H * DH;
     const float sl2 = a.scale * 1.4426950408889634f;
 
@@ -84,13 +90,13 @@ __global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
     const int nblk = (a.T + 31) >> 5;
     const int kb0 = split * a.bps, kb1 = min(nblk, kb0 + a.bps);
 
-    // stage block kb into buffer `buf`: slot s -> K plane / V^T plane position
+    // stage block kb into the group's buffer `buf`: slot s -> K plane / V^T plane position
     auto stage = [&](int kb, int buf) {
         const int k0 = kb * 32;
-        char* base = lds + buf * BUF;
+        char* base = lds + (grp * 2 + buf) * BUF;
 #pragma unroll
         for (int j = 0; j < (NSLOT / 64 + QG - 1) / QG; ++j) {
-            const int i = wave + j * QG;
+            const int i = qw + j * QG;
             if (i >= NSLOT / 64) break;
             const int sl = i * 64 + lane;
             const uint16_t* src;
@@ -108,7 +114,7 @@ __global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
         }
     };
 
-    if (kb0 < kb1) stage(kb0, 0);
+    if (kb0 + grp < kb1) stage(kb0 + grp, 0);
 
     u32x4_t qf[NC][2];
 #pragma unroll
@@ -125,12 +131,17 @@ __global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
     for (int dt = 0; dt < ND; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const int krow0 = 8 * (r >> 2) + (r & 3);   // + 4t: the key this lane reads for tile t
 
-    for (int kb = kb0; kb < kb1; ++kb) {
-        const int cur = (kb - kb0) & 1;
+    // every group runs the same number of rounds (the barriers line up); a group
+    // whose block lies past the split's range only stages and waits
+    const int rounds = (max(kb1 - kb0, 0) + KS - 1) / KS;
+    for (int t = 0; t < rounds; ++t) {
+        const int kb = kb0 + grp + t * KS;
+        const int cur = t & 1;
         __builtin_amdgcn_s_waitcnt(0);          // this wave's loads into `cur` have landed
         __syncthreads();                        // ... and everyone's; `cur ^ 1` is free again
-        if (kb + 1 < kb1) stage(kb + 1, cur ^ 1);
-        const char* Kb = lds + cur * BUF;
+        if (kb + KS < kb1) stage(kb + KS, cur ^ 1);
+        if (kb >= kb1) continue;
+        const char* Kb = lds + (grp * 2 + cur) * BUF;
         const char* Vb = Kb + KPLANE;
         const int k0 = kb * 32;
 
@@ -204,6 +215,54 @@ __global__ void __launch_bounds__(QG * 64) attn_f16_kernel(AttnArgs a) {
     float l = lrun;
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
+    if constexpr (KS > 1) {
+        // merge the key groups in group order: O = sum_k o_k 2^(m_k - M), L = sum_k l_k 2^(m_k - M)
+        __syncthreads();                        // every group is done with its staging buffers
+        float* o_sm = (float*)lds;              // [KS][QG * 16][MLD]
+        float* m_sm = o_sm + KS * QG * 16 * MLD;
+        float* l_sm = m_sm + KS * QG * 16;
+        const int rec = grp * QG * 16 + qw * 16 + r;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o_sm[rec * MLD + 16 * dt + 4 * g + i] = oacc[dt][i];
+        if (g == 0) {
+            m_sm[rec] = mrun;
+            l_sm[rec] = l;
+        }
+        __syncthreads();
+        const int row0 = blockIdx.z * 16 * QG;
+        for (int idx = threadIdx.x; idx < QG * 16 * (DH / 4); idx += blockDim.x) {
+            const int q = idx / (DH / 4), d0 = 4 * (idx % (DH / 4));
+            float mx = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < KS; ++k) mx = fmaxf(mx, m_sm[k * QG * 16 + q]);
+            float L = 0.f;
+            float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int k = 0; k < KS; ++k) {
+                const float mk = m_sm[k * QG * 16 + q];
+                const float e = (mk == -INFINITY) ? 0.f : exp2f(mk - mx);
+                const float* ok = o_sm + (k * QG * 16 + q) * MLD + d0;
+                L += l_sm[k * QG * 16 + q] * e;
+                o.x += ok[0] * e; o.y += ok[1] * e; o.z += ok[2] * e; o.w += ok[3] * e;
+            }
+            if (a.nsplit == 1) {
+                const float inv = 1.f / L;
+                xfrag_store4<false>(a.o, row0 + q, h * DH + d0, a.KCx,
+                                    make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv));
+            } else {
+                float* op = a.opart + (((size_t)split * a.rows_ld + row0 + q) * a.H + h) * DH;
+                *(float4*)(op + d0) = o;
+                if (d0 == 0) {
+                    float* ml = a.mlpart + (((size_t)split * a.rows_ld + row0 + q) * a.H + h) * 2;
+                    ml[0] = mx;
+                    ml[1] = L;
+                }
+            }
+        }
+        return;
+    }
     if (a.nsplit == 1) {
         const float inv = 1.f / l;
 #pragma unroll

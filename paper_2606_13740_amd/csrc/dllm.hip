@@ -93,6 +93,12 @@ struct Workspace {
 };
 
 constexpr int MAX_SPLIT = 16;
+// Windows of <= 64 rows: most 32-key blocks one attention key group streams before the
+// key range is split across workgroups (and merged by a separate launch).
+#ifndef ATTN_ROUNDS
+#define ATTN_ROUNDS 3
+#endif
+constexpr int ATTN_KEYGROUP_BLOCKS = 48;
 constexpr int RES_SPLIT = 4;     // K slices of the O / down projections for windows of <= 64 rows
 
 }  // namespace
@@ -651,6 +657,31 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 if (Dh == 32) hipLaunchKernelGGL((attn_f32_kernel<32>), dim3(Mc, H), dim3(64), 0, s, at);
                 else if (Dh == 64) hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(Mc, H), dim3(64), 0, s, at);
                 else hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(Mc, H), dim3(64), 0, s, at);
+            } else if (gy == 1 && Mc >= 48 && ceil_div(a.T, 32) <= ATTN_KEYGROUP_BLOCKS) {
+                // windows of 48-64 rows over up to 1536 keys: the workgroup's QG query tiles
+                // share each staged block and KS = 2 key groups take alternate blocks
+                // (8 waves stage 2 blocks at a time); key splits across workgroups where a
+                // group would take more than ATTN_ROUNDS blocks.  LLaDA-8B, 64 rows,
+                // prefix 1024: 17.5 against 20.0 us per layer for one key group.  For 32
+                // rows, and for long prefixes, one group per workgroup and the most splits
+                // are faster (prefix 512: 13.3 against 14.9-15.8 us; 4096: 32.4 against 34.1).
+                const int QGs = Mc / 16;
+                const int KSs = QGs <= 2 ? 4 : 2;
+                const int nblk = ceil_div(a.T, 32);
+                int nsplit = std::min(ceil_div(nblk, KSs * ATTN_ROUNDS), MAX_SPLIT);
+                at.bps = ceil_div(nblk, nsplit);
+                at.nsplit = ceil_div(nblk, at.bps);
+                dim3 grid(at.nsplit, H, 1);
+#define ATTN_W(DH_, QG_, KS_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, KS_>), grid, dim3(QG_ * KS_ * 64), 0, s, at)
+#define ATTN_W_QG(DH_) \
+    do { if (QGs == 1) ATTN_W(DH_, 1, 4); else if (QGs == 2) ATTN_W(DH_, 2, 4); \
+         else if (QGs == 3) ATTN_W(DH_, 3, 2); else ATTN_W(DH_, 4, 2); } while (0)
+                if (Dh == 128) ATTN_W_QG(128); else ATTN_W_QG(64);
+#undef ATTN_W_QG
+#undef ATTN_W
+                if (at.nsplit > 1)
+                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(Mc * H, 8)), dim3(256), 0, s, at,
+                                       Mc, Dh);
             } else {
                 // QG query tiles share each staged K/V block; key splits across
                 // workgroups give the chip enough waves (~2 per SIMD) and are merged
@@ -668,7 +699,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
                 dim3 grid(at.nsplit, H, nqg);
-#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_>), grid, dim3(QG_ * 64), 0, s, at)
+#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, 1>), grid, dim3(QG_ * 64), 0, s, at)
 #define ATTN_QG(DH_) \
     do { if (QG == 8) ATTN(DH_, 8); else if (QG == 4) ATTN(DH_, 4); else if (QG == 3) ATTN(DH_, 3); \
          else if (QG == 2) ATTN(DH_, 2); \
