@@ -524,6 +524,27 @@ def measured_read_peak(dl, torch, dev, gib=4):
     return buf_gbs(gib << 30, best)
 
 
+def read_floor_us(dl, torch, dev, nbytes, pool):
+    """Mean duration of the library's plain streaming read over `nbytes` (the same
+    16-byte non-temporal loads the GEMMs use), launched back to back over consecutive
+    windows of a >= 2 GiB pool (so the 256 MB Infinity Cache cannot serve them): the
+    floor a kernel that only reads that many bytes reaches, its launch included."""
+    n16 = (int(nbytes) + 15) // 16 * 16
+    nwin = max(1, pool.numel() // n16)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    base = pool.data_ptr()
+    for i in range(4):
+        dl.lib().dllm_read_bandwidth(base + (i % nwin) * n16, n16, sink.data_ptr(), None)
+    n = 32
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n):
+        dl.lib().dllm_read_bandwidth(base + (i % nwin) * n16, n16, sink.data_ptr(), None)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / n
+
+
 def buf_gbs(nbytes, ms):
     return nbytes / (ms * 1e-3) / 1e9
 
@@ -720,6 +741,14 @@ def main():
     step()                          # leave the workspaces as a step leaves them
     torch.cuda.synchronize()
     read_gbs = measured_read_peak(dl, torch, dev)
+    # per-size floor: a plain read of each class's algorithmic bytes
+    pool = torch.empty(max(2 << 30, int(4.2 * max(v["alg_bytes"] for v in kern.values()))), dtype=torch.uint8,
+                       device=dev)
+    for name, v in kern.items():
+        f = read_floor_us(dl, torch, dev, v["alg_bytes"], pool)
+        v["read_floor_us"] = f
+        v["frac_of_read_floor"] = f / v["mean_us"] if v["mean_us"] > 0 else None
+    del pool
     dom = "gateup"
     dk = kern[dom]
     traffic = measured_traffic(args.workload)
