@@ -77,8 +77,17 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int grp = wave / QG, qw = wave % QG;                // key group, query tile
-    const int split = blockIdx.x, h = blockIdx.y;
-    const int row = blockIdx.z * 16 * QG + 16 * qw + r;      // this lane's query row
+    // 1-D grid over (head h, query group z, split) items, in that order.  The dispatcher
+    // deals consecutive workgroups to the 8 XCDs in turn; when the items divide into
+    // 8 equal shares, XCD x takes the x-th share, so the query groups and splits of a
+    // head (which read the same K/V, the splits adjacent 64-byte halves of the same
+    // V^T lines) share one L2.
+    const int nitems = (int)gridDim.x;
+    const int nqg = nitems / (a.nsplit * a.H);
+    int item = blockIdx.x;
+    if ((nitems & 7) == 0) item = (blockIdx.x & 7) * (nitems >> 3) + (blockIdx.x >> 3);
+    const int split = item % a.nsplit, z = (item / a.nsplit) % nqg, h = item / (a.nsplit * nqg);
+    const int row = z * 16 * QG + 16 * qw + r;               // this lane's query row
     const int ld = a.H * DH;
     const float sl2 = a.scale * 1.4426950408889634f;
 
@@ -231,7 +240,7 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
             l_sm[rec] = l;
         }
         __syncthreads();
-        const int row0 = blockIdx.z * 16 * QG;
+        const int row0 = z * 16 * QG;
         for (int idx = threadIdx.x; idx < QG * 16 * (DH / 4); idx += blockDim.x) {
             const int q = idx / (DH / 4), d0 = 4 * (idx % (DH / 4));
             float mx = -INFINITY;

@@ -671,7 +671,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 int nsplit = std::min(ceil_div(nblk, KSs * ATTN_ROUNDS), MAX_SPLIT);
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
-                dim3 grid(at.nsplit, H, 1);
+                dim3 grid(at.nsplit * H);
 #define ATTN_W(DH_, QG_, KS_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, KS_>), grid, dim3(QG_ * KS_ * 64), 0, s, at)
 #define ATTN_W_QG(DH_) \
     do { if (QGs == 1) ATTN_W(DH_, 1, 4); else if (QGs == 2) ATTN_W(DH_, 2, 4); \
@@ -698,7 +698,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 nsplit = std::min(nsplit, MAX_SPLIT);
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
-                dim3 grid(at.nsplit, H, nqg);
+                dim3 grid(at.nsplit * H * nqg);
 #define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, 1>), grid, dim3(QG_ * 64), 0, s, at)
 #define ATTN_QG(DH_) \
     do { if (QG == 8) ATTN(DH_, 8); else if (QG == 4) ATTN(DH_, 4); else if (QG == 3) ATTN(DH_, 3); \
