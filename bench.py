@@ -611,6 +611,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT,
                     choices=sorted(WORKLOADS) + [E2E, E2E_STAGED, E2E_MERGED, E2E_MBSD] + sorted(PREFILL))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="default workload: skip the end-to-end, tiny-model, M-sweep and read-floor measurements "
+                         "(short runs under a counter profiler)")
     ap.add_argument("--no-sls", action="store_true",
                     help="run the LM head over every window row (no selective logits skipping)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -661,7 +664,7 @@ def main():
     glob = synth.global_weights(shape, "bf16")
     # the default workload's model also serves the end-to-end generation (prompt 512 +
     # 128 tokens) and the down-projection M-sweep (windows up to 256 rows)
-    extras = args.workload == DEFAULT
+    extras = args.workload == DEFAULT and not args.no_extras
     model = dl.Model(shape, dtype, glob, lambda l: synth.layer_weights(shape, l, "bf16"),
                      max_window=256 if extras else 64, max_pos=max(P + W + 64, 1024 if extras else 0))
     log(f"model created in {time.time() - t0:.1f} s")
@@ -742,9 +745,13 @@ def main():
     torch.cuda.synchronize()
     read_gbs = measured_read_peak(dl, torch, dev)
     # per-size floor: a plain read of each class's algorithmic bytes
-    pool = torch.empty(max(2 << 30, int(4.2 * max(v["alg_bytes"] for v in kern.values()))), dtype=torch.uint8,
-                       device=dev)
+    pool = None
+    if not args.no_extras:
+        pool = torch.empty(max(2 << 30, int(4.2 * max(v["alg_bytes"] for v in kern.values()))), dtype=torch.uint8,
+                           device=dev)
     for name, v in kern.items():
+        if pool is None:
+            break
         f = read_floor_us(dl, torch, dev, v["alg_bytes"], pool)
         v["read_floor_us"] = f
         v["frac_of_read_floor"] = f / v["mean_us"] if v["mean_us"] > 0 else None
