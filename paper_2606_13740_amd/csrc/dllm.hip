@@ -232,14 +232,15 @@ bool wide_layout(GemmKind k, int wt, int gy) {
 // the LM head takes 4, since at 8 its code pipeline, activations and 16
 // accumulators per token tile need more than 256 registers and leave one wave per
 // SIMD (LLaDA-8B vocabulary at 32 rows: 119 against 144 us per launch); the
-// gate/up takes 3 past 2 token tiles, where 6 would spill.  bf16 split-K projections
+// gate/up and the split-K projections take 3 past 2 token tiles, where 6 (gate/up)
+// or 4 (down: 47 registers at 4 token tiles) would spill.  bf16 split-K projections
 // up to 2 token tiles (the down projection of windows of <= 32 rows) take 8 tiles
 // over 8 K slices instead of 4 over 4: the same 256 workgroups, but every workgroup
 // re-reads the hi/lo activation operand of its K slice through L2, so twice the
 // rows per workgroup halve that traffic (LLaDA-8B down at 32 rows: 28.6 -> 26.8 us
 // per launch with the reduction, against twice the partial sums).
 constexpr int template_fw(GemmKind k, int wt, int mt) {
-    if (wt == WT_Q4 && k == G_GU && mt >= 3) return 3;
+    if (wt == WT_Q4 && (k == G_GU || k == G_RES) && mt >= 3) return 3;
     if (wt == WT_BF16 && k == G_RES && mt <= 2) return 8;
     return k == G_QKV ? 3 : (k == G_GU ? 6 : (k == G_LM ? (wt == WT_Q4 ? 4 : 8) : 4));
 }

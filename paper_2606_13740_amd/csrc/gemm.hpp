@@ -76,6 +76,11 @@ constexpr int pipeline_depth() {
             return d < 1 ? 1 : (d > 8 ? 8 : d);
         }
     }
+    // bf16 at 3-4 token tiles (row groups of 2-6 tiles): the activation stages take
+    // most of the registers (2 planes x MT tiles), so one activation stage (L2-resident)
+    // beside 3-4 weight stages (HBM) instead of 2-3 of each (activation_depth);
+    // LLaDA-8B, 64-row window at prefix 1024: 5.25 -> 5.16 ms per step
+    if constexpr (WT == WT_BF16 && MT >= 3 && F > 1 && F < 8) return (MT == 4 || F == 6) ? 3 : 4;
     constexpr int slot = 4 * (F + MT * WTraits<WT>::XPER * XP);
     constexpr int d = 128 / slot;
     return d < 1 ? 1 : (d > 8 ? 8 : d);
@@ -85,10 +90,14 @@ constexpr int pipeline_depth() {
 // pipeline runs deeper than its activations (L2-resident, 16 dwords per token tile
 // and stage): one stage, which leaves the registers for 6 row tiles per wave
 // (LLaDA-8B gate/up at 32 rows: 23.6 us per launch against 33.5 with 3 tiles and
-// two activation stages).
+// two activation stages); and bf16 at 3-4 token tiles (pipeline_depth).
 template <int WT, int F, int MT>
 constexpr int activation_depth() {
     if constexpr (WT == WT_Q4) return 1;
+    if constexpr (WT == WT_BF16 && MT >= 3 && F > 1 && F < 8) return (MT == 4 || F == 6) ? 1 : 2;
+    // the 10-tile gate/up (Dream-7B widths): one activation stage beside two weight
+    // stages; with two of each it spilled (gate/up 53.4 -> 51.4 us, step 3.95 -> 3.85 ms)
+    if constexpr (WT == WT_BF16 && F == 10 && MT <= 2) return 1;
     if constexpr (F == 1 && (WT == WT_BF16 || WT == WT_I8)) {
         // ~64 VGPRs of activation stages (hi + lo planes, XPER 32-column halves)
         constexpr int per = 4 * WTraits<WT>::XPER * 2 * MT;
