@@ -60,8 +60,12 @@ __device__ __forceinline__ int swz_k(int key) { return (key & 3) | (((key >> 3) 
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// At most two waves per SIMD's worth of registers (256): with the 512 a workgroup of
+// 2-4 waves may take, the compiler chose the AGPR form of the MFMAs and copied every
+// output tile VGPR -> AGPR around each product.
 template <int DH, int QG, int KS>
-__global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(QG * KS * 64) __attribute__((amdgpu_waves_per_eu(2)))
+attn_f16_kernel(AttnArgs a) {
     constexpr int NC = DH / 32;               // 32-dim chunks
     constexpr int ND = DH / 16;               // 16-dim output tiles
     constexpr int KCOLS = DH / 8;             // 16-byte columns per key row
@@ -133,6 +137,10 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
         qf[c][1] = ldg16(src + a.q_plane);
     }
     const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
+    // smallest key limit of the wave's rows: blocks below it need no per-key mask
+    int lim_w = lim;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) lim_w = min(lim_w, __shfl_xor(lim_w, o));
 
     float mrun = -INFINITY, lrun = 0.f;
     f32x4_t oacc[ND];
@@ -169,11 +177,19 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
         }
 
         float sv[8];
+        if (k0 + 32 <= lim_w) {                 // every key of the block is visible to every row
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int key0 = k0 + 8 * g + i, key1 = key0 + 4;
-            sv[i] = (key0 < lim) ? s0[i] * sl2 : -INFINITY;
-            sv[4 + i] = (key1 < lim) ? s1[i] * sl2 : -INFINITY;
+            for (int i = 0; i < 4; ++i) {
+                sv[i] = s0[i] * sl2;
+                sv[4 + i] = s1[i] * sl2;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int key0 = k0 + 8 * g + i, key1 = key0 + 4;
+                sv[i] = (key0 < lim) ? s0[i] * sl2 : -INFINITY;
+                sv[4 + i] = (key1 < lim) ? s1[i] * sl2 : -INFINITY;
+            }
         }
         float bm = sv[0];
 #pragma unroll
@@ -184,10 +200,13 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
         float alpha = 1.f, ps = 0.f;
         uint32_t phi[4] = {0u, 0u, 0u, 0u}, plo[4] = {0u, 0u, 0u, 0u};
         if (mnew != -INFINITY) {
-            alpha = exp2f(mrun - mnew);
+            // v_exp_f32 directly: the arguments are <= 0 (or -inf), so the results lie
+            // in [0, 1] and only those below 2^-126 (flushed to zero) differ from exp2f
+            alpha = __builtin_amdgcn_exp2f(mrun - mnew);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float p0 = exp2f(sv[2 * e] - mnew), p1 = exp2f(sv[2 * e + 1] - mnew);
+                const float p0 = __builtin_amdgcn_exp2f(sv[2 * e] - mnew);
+                const float p1 = __builtin_amdgcn_exp2f(sv[2 * e + 1] - mnew);
                 ps += p0 + p1;
                 // p in [0, 1]: hi = fp16 toward zero, lo = the remainder toward zero
                 const auto h = __builtin_amdgcn_cvt_pkrtz(p0, p1);
@@ -200,7 +219,18 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
         mrun = mnew;
         const u32x4_t ph = {phi[0], phi[1], phi[2], phi[3]};
         const u32x4_t pl = {plo[0], plo[1], plo[2], plo[3]};
-        const bool tail = (k0 + 8 * g + 8 > a.T);
+        // V beyond T is zeroed (those cache rows may be unwritten): only the block that
+        // holds T, a decision uniform over the workgroup; the lane's keep masks are the
+        // same for every output tile
+        uint32_t keep[4] = {~0u, ~0u, ~0u, ~0u};
+        const bool tail = (k0 + 32 > a.T);
+        if (tail) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int key = k0 + 8 * g + 2 * e;
+                keep[e] = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
+            }
+        }
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
 #pragma unroll
@@ -208,13 +238,9 @@ __global__ void __launch_bounds__(QG * KS * 64) attn_f16_kernel(AttnArgs a) {
             const int dim = 16 * dt + r;
             const int off = dim * 64 + ((g ^ ((dim >> 2) & 3)) << 4);
             u32x4_t vf = *(const u32x4_t*)(Vb + off);
-            if (tail) {                          // zero V beyond T (those rows may be unwritten)
+            if (tail) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int key = k0 + 8 * g + 2 * e;
-                    const uint32_t keep = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
-                    vf[e] &= keep;
-                }
+                for (int e = 0; e < 4; ++e) vf[e] &= keep[e];
             }
             oacc[dt] = mfma_f16(vf, ph, oacc[dt]);
             oacc[dt] = mfma_f16(vf, pl, oacc[dt]);
@@ -347,6 +373,10 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
     const float* Kp = (const float*)a.K + (size_t)hk * a.Cs * DH;
     const float* Vp = (const float*)a.Vt + (size_t)hk * DH * a.Cs;
     const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
+    // smallest key limit of the wave's rows: blocks below it need no per-key mask
+    int lim_w = lim;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) lim_w = min(lim_w, __shfl_xor(lim_w, o));
 
     float q[DH];
 #pragma unroll
