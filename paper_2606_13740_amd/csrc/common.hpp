@@ -146,9 +146,11 @@ __device__ __forceinline__ u32x4_t i8x8_to_bf16x8(uint32_t lo, uint32_t hi) {
         for (int p = 0; p < 2; ++p) {
             const int b0 = (int)(int8_t)((w[j] >> (16 * p)) & 0xFF);
             const int b1 = (int)(int8_t)((w[j] >> (16 * p + 8)) & 0xFF);
-            const uint32_t f0 = __float_as_uint((float)b0) >> 16;
-            const uint32_t f1 = __float_as_uint((float)b1) >> 16;
-            r[2 * j + p] = f0 | (f1 << 16);
+            // the high halves of the two floats (exact: |b| <= 128 needs 8 bits), packed
+            // by one byte permute: bytes 2-3 of f0, then bytes 2-3 of f1
+            const uint32_t f0 = __float_as_uint((float)b0);
+            const uint32_t f1 = __float_as_uint((float)b1);
+            r[2 * j + p] = __builtin_amdgcn_perm(f1, f0, 0x07060302u);
         }
     }
     return r;
