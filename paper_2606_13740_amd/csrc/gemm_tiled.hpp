@@ -167,7 +167,7 @@ __global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, in
         epi.fetch(pre, nt0 * 16, nrows, mtp * 16, mcols);
         epi.stage(pre, esm, nt0 * 16, nrows, mtp * 16, mcols);
         __syncthreads();
-        epi(Y, T::LDY, nt0 * 16, nrows, mtp * 16, mcols, blockIdx.x, esm);
+        epi(Y, T::LDY, nt0 * 16, nrows, mtp * 16, mcols, blockIdx.x, esm, NoScale{});
         __syncthreads();
     }
 }
