@@ -566,7 +566,7 @@ def measured_traffic(workload):
         if DOMINANT in line:
             parts = line.split()
             try:
-                return (float(parts[-2]) + float(parts[-1])) * 1e6
+                return round((float(parts[-2]) + float(parts[-1])) * 1e6)
             except ValueError:
                 return None
     return None
