@@ -373,10 +373,6 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
     const float* Kp = (const float*)a.K + (size_t)hk * a.Cs * DH;
     const float* Vp = (const float*)a.Vt + (size_t)hk * DH * a.Cs;
     const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
-    // smallest key limit of the wave's rows: blocks below it need no per-key mask
-    int lim_w = lim;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) lim_w = min(lim_w, __shfl_xor(lim_w, o));
 
     float q[DH];
 #pragma unroll

@@ -58,17 +58,18 @@ struct GemmArgs {
 // it (it may use __syncthreads and overwrite Y); `part` numbers the row group for
 // per-group partial results.
 
-// The scales of a tile's outputs, applied where an epilogue reads Y: a separate pass
-// over Y, with its barrier and its per-element loads of the row scales from global
-// memory, made the int8 LM head 170 us instead of 159 and the int8 64-row window at
-// prefix 4096 4.90 ms instead of 4.74.  The row scales and biases are staged in LDS
-// while the weights stream.  Per output:
-// y * ws[nl] (int8 row scale), * rs[ml] (folded RMSNorm), + b[nl] (bias); each
-// pointer is to LDS, or nullptr when that scale is absent.
 // No scales at all (most bf16 launches): the epilogues read the sums unchanged.
 struct NoScale {
     __device__ __forceinline__ float operator()(float y, int, int) const { return y; }
 };
+
+// The scales of a tile's outputs, applied where an epilogue reads Y: a separate pass
+// over Y, with its barrier and its per-element loads of the row scales from global
+// memory, made the int8 LM head 170 us instead of 159 and the int8 64-row window at
+// prefix 4096 4.90 ms instead of 4.74.  The row scales and biases are staged in LDS
+// while the weights stream.  Per output: y * ws[nl] (int8 row scale), * rs[ml] (folded
+// RMSNorm), + b[nl] (bias); each pointer is to LDS, or nullptr when that scale is
+// absent.
 struct YScale {
     const float* ws = nullptr;
     const float* rs = nullptr;
