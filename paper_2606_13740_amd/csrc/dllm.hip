@@ -687,7 +687,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
 #undef ATTN_W_QG
 #undef ATTN_W
                 if (at.nsplit > 1)
-                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(Mc * H, 8)), dim3(256), 0, s, at,
+                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(Mc * H, ATTN_MERGE_PAIRS)),
+                                       dim3(32 * ATTN_MERGE_PAIRS), 0, s, at,
                                        Mc, Dh);
             } else {
                 // QG query tiles share each staged K/V block; key splits across
@@ -715,7 +716,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
 #undef ATTN_QG
 #undef ATTN
                 if (at.nsplit > 1) {
-                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(Mc * H, 8)), dim3(256), 0, s, at,
+                    hipLaunchKernelGGL((attn_combine_kernel<false>), dim3(ceil_div(Mc * H, ATTN_MERGE_PAIRS)),
+                                       dim3(32 * ATTN_MERGE_PAIRS), 0, s, at,
                                        Mc, Dh);
                 }
             }
