@@ -46,8 +46,8 @@ struct AttnArgs {
 // Workgroup = (key split, head, group of QG query tiles of 16 rows), KS x QG waves:
 // KS key groups of QG waves, one wave per query tile.  Key group k takes the split's
 // 32-key blocks k, k + KS, ...; each block is staged in the group's own LDS buffers
-// once with direct global->LDS loads (global_load_lds_dwordx4), double-buffered so the
-// next block streams in while the current one is used, and the group's waves read
+// once with direct global->LDS loads (global_load_lds_dwordx4) in a ring of NB buffers,
+// so the next NB - 1 blocks stream in while the current one is used, and the group's waves read
 // their MFMA fragments from LDS.  With KS > 1 the groups' partial (max, sum, O)
 // states are merged in LDS in group order at the end.  LDS rows are XOR-swizzled in 16-byte columns so that
 // the 16 rows one fragment read touches fall in distinct banks:
@@ -63,7 +63,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 // At most two waves per SIMD's worth of registers (256): with the 512 a workgroup of
 // 2-4 waves may take, the compiler chose the AGPR form of the MFMAs and copied every
 // output tile VGPR -> AGPR around each product.
-template <int DH, int QG, int KS>
+// Staging buffers per workgroup with one key group (KS = 1).
+constexpr int ATTN_RING = 2;
+// log2-domain slack of the lazily rescaled softmax maximum: probabilities <= 2^8
+constexpr float ATTN_SLACK = 8.f;
+
+template <int DH, int QG, int KS, int NB>
 __global__ void __launch_bounds__(QG * KS * 64) __attribute__((amdgpu_waves_per_eu(2)))
 attn_f16_kernel(AttnArgs a) {
     constexpr int NC = DH / 32;               // 32-dim chunks
@@ -76,9 +81,11 @@ attn_f16_kernel(AttnArgs a) {
     static_assert(NSLOT % 64 == 0, "block must be whole wave loads");
     constexpr int MLD = DH + 4;               // merge: floats per (group, row) record
     constexpr int MERGE = KS > 1 ? KS * QG * 16 * (MLD + 2) * 4 : 0;
-    __shared__ __attribute__((aligned(1024))) char lds[KS * 2 * BUF > MERGE ? KS * 2 * BUF : MERGE];
+    static_assert(NB >= 2 && NB <= 4, "2-4 staging buffers per key group");
+    constexpr int LPW = (NSLOT / 64) / QG;    // loads each wave issues per staged block, at least
+    __shared__ __attribute__((aligned(1024))) char lds[KS * NB * BUF > MERGE ? KS * NB * BUF : MERGE];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15, g = lane >> 4;
     const int grp = wave / QG, qw = wave % QG;                // key group, query tile
     // 1-D grid over (head h, query group z, split) items, in that order.  The dispatcher
@@ -106,7 +113,7 @@ attn_f16_kernel(AttnArgs a) {
     // stage block kb into the group's buffer `buf`: slot s -> K plane / V^T plane position
     auto stage = [&](int kb, int buf) {
         const int k0 = kb * 32;
-        char* base = lds + (grp * 2 + buf) * BUF;
+        char* base = lds + (grp * NB + buf) * BUF;
 #pragma unroll
         for (int j = 0; j < (NSLOT / 64 + QG - 1) / QG; ++j) {
             const int i = qw + j * QG;
@@ -127,7 +134,30 @@ attn_f16_kernel(AttnArgs a) {
         }
     };
 
-    if (kb0 + grp < kb1) stage(kb0 + grp, 0);
+    // zero the V^T values of keys >= T in the slots this wave staged into buffer `buf`
+    // (cache rows past T may hold anything, and 0 * NaN would reach O); K needs no
+    // such care, its scores past T are masked
+    auto zero_tail = [&](int kb, int buf) {
+        const int k0 = kb * 32;
+        char* base = lds + (grp * NB + buf) * BUF;
+#pragma unroll
+        for (int j = 0; j < (NSLOT / 64 + QG - 1) / QG; ++j) {
+            const int i = qw + j * QG;
+            if (i >= NSLOT / 64) break;
+            const int sl = i * 64 + lane;
+            if (sl < KPLANE / 16) continue;
+            const int s1 = sl - KPLANE / 16;
+            const int dim = s1 >> 2, pc = s1 & 3;
+            const int key = k0 + 8 * (pc ^ ((dim >> 2) & 3));      // the slot's first key
+            if (key + 8 <= a.T) continue;
+            u32x4_t* slot = (u32x4_t*)(base + i * 1024 + lane * 16);
+            u32x4_t v = *slot;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] &= (key + 2 * e >= a.T ? 0u : 0x0000FFFFu) | (key + 2 * e + 1 >= a.T ? 0u : 0xFFFF0000u);
+            *slot = v;
+        }
+    };
 
     u32x4_t qf[NC][2];
 #pragma unroll
@@ -137,10 +167,26 @@ attn_f16_kernel(AttnArgs a) {
         qf[c][1] = ldg16(src + a.q_plane);
     }
     const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
-    // smallest key limit of the wave's rows: blocks below it need no per-key mask
-    int lim_w = lim;
+
+    // Ring of NB buffers per key group: the group's first NB - 1 blocks are staged
+    // here (after the Q loads, so the ring's waits below see only block loads after
+    // them), and round t stages its block t + NB - 1 into the buffer round t - 1 used.
+    // With one key group every split has a block, and a split shorter than NB - 1
+    // blocks stages its last one again into the spare buffers: unconditional loads
+    // keep the compiler's own wait for the limit loads below from covering the blocks.
+    const int nmine = kb0 + grp < kb1 ? (kb1 - kb0 - grp + KS - 1) / KS : 0;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) lim_w = min(lim_w, __shfl_xor(lim_w, o));
+    for (int j = 0; j < NB - 1; ++j) {
+        if constexpr (KS == 1) stage(kb0 + min(j, nmine - 1), j);
+        else if (j < nmine) stage(kb0 + grp + j * KS, j);
+    }
+
+    // smallest key limit of the wave's 16 rows (lanes 0-15 hold them): blocks below it
+    // need no per-key mask.  Read lane by lane into a scalar, so that the per-block
+    // test is a scalar branch.
+    int lim_w = __builtin_amdgcn_readlane(lim, 0);
+#pragma unroll
+    for (int i = 1; i < 16; ++i) lim_w = min(lim_w, __builtin_amdgcn_readlane(lim, i));
 
     float mrun = -INFINITY, lrun = 0.f;
     f32x4_t oacc[ND];
@@ -153,12 +199,23 @@ attn_f16_kernel(AttnArgs a) {
     const int rounds = (max(kb1 - kb0, 0) + KS - 1) / KS;
     for (int t = 0; t < rounds; ++t) {
         const int kb = kb0 + grp + t * KS;
-        const int cur = t & 1;
-        __builtin_amdgcn_s_waitcnt(0);          // this wave's loads into `cur` have landed
-        __syncthreads();                        // ... and everyone's; `cur ^ 1` is free again
-        if (kb + KS < kb1) stage(kb + KS, cur ^ 1);
+        const int cur = t % NB;
+        // this wave's loads of block t have landed once at most LPW per block staged
+        // after it are outstanding (loads complete in issue order, and the loop issues
+        // no other vector-memory operations); the barrier then makes every wave's
+        // loads visible and frees the buffer round t - 1 read.  No workgroup fence:
+        // with loads into LDS in flight it would wait for all of them.
+        const int after = min(NB - 2, nmine - 1 - t);
+        if (kb < kb1 && kb * 32 + 32 > a.T) {  // the block holding T: the group's last
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            zero_tail(kb, cur);                 // before the barrier, so no other wave reads first
+        }
+        if (NB > 3 && after >= 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPW) : "memory");
+        else if (NB > 2 && after >= 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPW) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (t + NB - 1 < nmine) stage(kb + (NB - 1) * KS, (t + NB - 1) % NB);
         if (kb >= kb1) continue;
-        const char* Kb = lds + (grp * 2 + cur) * BUF;
+        const char* Kb = lds + (grp * NB + cur) * BUF;
         const char* Vb = Kb + KPLANE;
         const int k0 = kb * 32;
 
@@ -176,72 +233,71 @@ attn_f16_kernel(AttnArgs a) {
             }
         }
 
+        // unscaled scores of keys k0 + 8g + j (j = 0..7); keys past a row's limit -> -inf
         float sv[8];
-        if (k0 + 32 <= lim_w) {                 // every key of the block is visible to every row
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            sv[i] = s0[i];
+            sv[4 + i] = s1[i];
+        }
+        if (k0 + 32 > lim_w) {                  // some row of the wave stops inside the block
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                sv[i] = s0[i] * sl2;
-                sv[4 + i] = s1[i] * sl2;
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key0 = k0 + 8 * g + i, key1 = key0 + 4;
-                sv[i] = (key0 < lim) ? s0[i] * sl2 : -INFINITY;
-                sv[4 + i] = (key1 < lim) ? s1[i] * sl2 : -INFINITY;
+                const int key0 = k0 + 8 * g + i;
+                if (key0 >= lim) sv[i] = -INFINITY;
+                if (key0 + 4 >= lim) sv[4 + i] = -INFINITY;
             }
         }
-        float bm = sv[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) bm = fmaxf(bm, sv[j]);
-        bm = fmaxf(bm, __shfl_xor(bm, 16));
-        bm = fmaxf(bm, __shfl_xor(bm, 32));
-        const float mnew = fmaxf(mrun, bm);
-        float alpha = 1.f, ps = 0.f;
-        uint32_t phi[4] = {0u, 0u, 0u, 0u}, plo[4] = {0u, 0u, 0u, 0u};
-        if (mnew != -INFINITY) {
-            // v_exp_f32 directly: the arguments are <= 0 (or -inf), so the results lie
-            // in [0, 1] and only those below 2^-126 (flushed to zero) differ from exp2f
-            alpha = __builtin_amdgcn_exp2f(mrun - mnew);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float p0 = __builtin_amdgcn_exp2f(sv[2 * e] - mnew);
-                const float p1 = __builtin_amdgcn_exp2f(sv[2 * e + 1] - mnew);
-                ps += p0 + p1;
-                // p in [0, 1]: hi = fp16 toward zero, lo = the remainder toward zero
-                const auto h = __builtin_amdgcn_cvt_pkrtz(p0, p1);
-                const auto l = __builtin_amdgcn_cvt_pkrtz(p0 - (float)h[0], p1 - (float)h[1]);
-                phi[e] = __builtin_bit_cast(uint32_t, h);
-                plo[e] = __builtin_bit_cast(uint32_t, l);
-            }
+        // the row's block maximum over its four lane groups (lanes l, l ^ 16, l ^ 32,
+        // l ^ 48): each swap hands a lane its partner's value, and max is symmetric
+        float bm = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                         fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+        {
+            const auto w32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(bm), __float_as_uint(bm), false, false);
+            bm = fmaxf(__uint_as_float(w32[0]), __uint_as_float(w32[1]));
+            const auto w16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(bm), __float_as_uint(bm), false, false);
+            bm = fmaxf(__uint_as_float(w16[0]), __uint_as_float(w16[1]));
         }
-        lrun = lrun * alpha + ps;
-        mrun = mnew;
+        const float bms = bm * sl2;             // log2-domain block maximum (sl2 > 0)
+        // Lazy rescaling: the reference maximum mrun moves only when some row of the
+        // wave exceeds it by more than ATTN_SLACK (and on a row's first unmasked key),
+        // so the probabilities stay <= 2^ATTN_SLACK and most blocks skip the rescale.
+        // O, l and m are exact for any reference value; the split merge uses the same m.
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(bms > mrun + ATTN_SLACK) != 0, 0)) {
+            const float mnew = fmaxf(mrun, bms);
+            const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(mrun - mnew);
+            lrun *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) oacc[dt][i] *= alpha;
+            mrun = mnew;
+        }
+        // a row with no unmasked key yet keeps m = -inf; its masked scores give p = 0
+        const float mref = (mrun == -INFINITY) ? 0.f : mrun;
+        float ps;
+        uint32_t phi[4], plo[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            // v_exp_f32 directly: the arguments are <= ATTN_SLACK (or -inf); results below
+            // 2^-126 (flushed to zero) are the only ones that differ from exp2f
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[2 * e], sl2, -mref));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[2 * e + 1], sl2, -mref));
+            ps = e ? ps + (p0 + p1) : p0 + p1;
+            // hi = fp16 toward zero, lo = the remainder toward zero
+            const auto h = __builtin_amdgcn_cvt_pkrtz(p0, p1);
+            const auto l = __builtin_amdgcn_cvt_pkrtz(p0 - (float)h[0], p1 - (float)h[1]);
+            phi[e] = __builtin_bit_cast(uint32_t, h);
+            plo[e] = __builtin_bit_cast(uint32_t, l);
+        }
+        lrun += ps;
         const u32x4_t ph = {phi[0], phi[1], phi[2], phi[3]};
         const u32x4_t pl = {plo[0], plo[1], plo[2], plo[3]};
-        // V beyond T is zeroed (those cache rows may be unwritten): only the block that
-        // holds T, a decision uniform over the workgroup; the lane's keep masks are the
-        // same for every output tile
-        uint32_t keep[4] = {~0u, ~0u, ~0u, ~0u};
-        const bool tail = (k0 + 32 > a.T);
-        if (tail) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int key = k0 + 8 * g + 2 * e;
-                keep[e] = (key >= a.T ? 0u : 0x0000FFFFu) | (key + 1 >= a.T ? 0u : 0xFFFF0000u);
-            }
-        }
+        // (V^T of keys past T was zeroed when the block holding T was staged)
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) oacc[dt][i] *= alpha;
             const int dim = 16 * dt + r;
-            const int off = dim * 64 + ((g ^ ((dim >> 2) & 3)) << 4);
-            u32x4_t vf = *(const u32x4_t*)(Vb + off);
-            if (tail) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) vf[e] &= keep[e];
-            }
+            const u32x4_t vf = *(const u32x4_t*)(Vb + dim * 64 + ((g ^ ((dim >> 2) & 3)) << 4));
             oacc[dt] = mfma_f16(vf, ph, oacc[dt]);
             oacc[dt] = mfma_f16(vf, pl, oacc[dt]);
         }

@@ -679,7 +679,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
                 dim3 grid(at.nsplit * H);
-#define ATTN_W(DH_, QG_, KS_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, KS_>), grid, dim3(QG_ * KS_ * 64), 0, s, at)
+#define ATTN_W(DH_, QG_, KS_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, KS_, 2>), grid, dim3(QG_ * KS_ * 64), 0, s, at)
 #define ATTN_W_QG(DH_) \
     do { if (QGs == 1) ATTN_W(DH_, 1, 4); else if (QGs == 2) ATTN_W(DH_, 2, 4); \
          else if (QGs == 3) ATTN_W(DH_, 3, 2); else ATTN_W(DH_, 4, 2); } while (0)
@@ -707,7 +707,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 at.bps = ceil_div(nblk, nsplit);
                 at.nsplit = ceil_div(nblk, at.bps);
                 dim3 grid(at.nsplit * H * nqg);
-#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, 1>), grid, dim3(QG_ * 64), 0, s, at)
+#define ATTN(DH_, QG_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, 1, ATTN_RING>), grid, dim3(QG_ * 64), 0, s, at)
 #define ATTN_QG(DH_) \
     do { if (QG == 8) ATTN(DH_, 8); else if (QG == 4) ATTN(DH_, 4); else if (QG == 3) ATTN(DH_, 3); \
          else if (QG == 2) ATTN(DH_, 2); \
