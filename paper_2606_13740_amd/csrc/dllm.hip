@@ -192,7 +192,9 @@ constexpr int GU_WIDE_TILES = 10;
 // rows: gate/up 201 against 276 us, down 107 against 173; at 4096 rows gate/up 1063
 // against 2825, QKV 823 against 1735).  With fewer workgroups the streaming layouts
 // win (QKV at 512 rows, 96 tiles: 238 against 201 us; every GEMM of a 256-row
-// window).  Models below the streaming
+// window), except that bf16 QKV of up to 682 rows splits K in two when that reaches
+// TILED_MIN_WG (tiled_ks; LLaDA-8B at 512 rows: 192 workgroups, 192 -> 117 us per
+// layer with the split_epilogue_kernel finish).  Models below the streaming
 // layouts' thresholds (test sizes) take it whenever it applies: it accepts any row
 // and token tile counts (ragged tiles are clamped).  The residual projections split
 // K until the chip holds ~256 workgroups (O/down at 512 rows: 32 tiles x 8 slices);
@@ -207,8 +209,15 @@ bool tiled_layout(GemmKind k, int wt, int Mc) {
 // token tiles per workgroup of the tiled kernel
 int tiled_tt(int wt) { return wt == WT_I8 ? TiledShape<WT_I8>::TT : TiledShape<WT_BF16>::TT; }
 int tiled_ks(GemmKind k, int wt, int n_tiles, int Mc) {
-    if (k != G_RES) return 1;
     const long wgs = (long)ceil_div(n_tiles, 16) * ceil_div(Mc / 16, tiled_tt(wt));
+    if (k == G_QKV) {
+        // bf16 QKV of short prompts: two K slices when one leaves fewer than
+        // TILED_MIN_WG workgroups and two fit the chip (LLaDA-8B at 512 rows: 96 -> 192),
+        // finished by split_epilogue_kernel; two slices of an output at most 3 d wide
+        // fit the partial buffer up to 682 rows
+        return (wt == WT_BF16 && wgs < TILED_MIN_WG && 2 * wgs <= N_CU && 6 * Mc <= 4096) ? 2 : 1;
+    }
+    if (k != G_RES) return 1;
     int ks = 1;
     while (ks < 8 && wgs * ks * 2 <= N_CU && (long)ks * 2 * Mc <= 4096) ks *= 2;
     return ks;
@@ -305,7 +314,8 @@ int launch_gemm_mt(int MT, const GemmArgs& g, const Epi& epi, int n_tiles, int K
 int row_groups(const Decomp& dc, int n_tiles) { return ceil_div(n_tiles, dc.tpg); }
 
 template <int WT, GemmKind KIND, class Epi>
-int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const Epi& epi, int gy, hipStream_t s) {
+int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const Epi& epi, int gy, hipStream_t s,
+                float* part = nullptr, size_t part_floats = 0) {
     GemmArgs g = g0;
     g.tpg = dc.tpg;
     if constexpr ((WT == WT_BF16 && KIND != G_LM) || (WT == WT_I8 && KIND == G_QKV)) {
@@ -314,6 +324,23 @@ int launch_gemm(const Decomp& dc, int n_tiles, int MT, const GemmArgs& g0, const
             const int Mc = gy * MT * 16;
             if (Mc % 64 != 0) return fail(DLLM_E_INVAL, "internal: tiled GEMM needs 64-row blocks");
             dim3 grid(ceil_div(n_tiles, TS::RT), dc.ks, ceil_div(Mc / 16, TS::TT));
+            if constexpr (KIND == G_QKV && WT == WT_BF16) {
+                if (dc.ks > 1) {
+                    // K slices into partial sums, then split_epilogue_kernel sums them and
+                    // runs the QKV epilogue (the bias goes in once, after the sum)
+                    const int N = n_tiles * 16;
+                    if (part == nullptr || (size_t)dc.ks * Mc * N > part_floats)
+                        return fail(DLLM_E_INVAL, "internal: split-K buffer too small");
+                    GemmArgs gp = g0;
+                    gp.bias = nullptr;
+                    const EpiPartial ep{part, N, Mc};
+                    hipLaunchKernelGGL((gemm_tiled_kernel<WT, EpiPartial>), grid, dim3(512), 0, s, gp, ep, Mc / 16);
+                    hipLaunchKernelGGL((split_epilogue_kernel<Epi>), dim3(ceil_div(n_tiles, 16), ceil_div(Mc / 16, 4)),
+                                       dim3(256), 0, s, (const float*)part, dc.ks, Mc, N, n_tiles, Mc / 16, g0.bias,
+                                       epi);
+                    return DLLM_OK;
+                }
+            }
             hipLaunchKernelGGL((gemm_tiled_kernel<WT, Epi>), grid, dim3(512), 0, s, g0, epi, Mc / 16);
             return DLLM_OK;
         }
@@ -648,7 +675,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
             if (fused && (l == 0 || FUSE_DOWN)) fold_norm(g, m, w, nssq_qkv(l));
             EpiQKV<XF32> e{d, m->dkv, Dh, a.M, a.pos_base, a.pos, m->rope, (AT*)w.q, q_plane, Kc, Vt, kv->Cs};
             ProbeScope ps(m, DLLM_K_QKV, s);
-            if ((rc = launch_gemm<WT, G_QKV>(decomp(G_QKV, WT, L.qkv.n_tiles, Mc, gy), L.qkv.n_tiles, MT, g, e, gy, s)))
+            if ((rc = launch_gemm<WT, G_QKV>(decomp(G_QKV, WT, L.qkv.n_tiles, Mc, gy), L.qkv.n_tiles, MT, g, e, gy, s,
+                                             w.part, w.part_floats)))
                 return rc;
         }
         // attention over [0, T) (+ split merge)

@@ -172,4 +172,45 @@ __global__ void __launch_bounds__(512) gemm_tiled_kernel(GemmArgs g, Epi epi, in
     }
 }
 
+// Split-K finish of the tiled kernel for the QKV projection of short prompts (whose
+// 256 x 256 tiles alone leave the chip half idle): each workgroup sums the KS partial
+// slices P[s][m][n] of a 256-row x 64-token block in slice order into an LDS tile,
+// adds the bias once, and runs the projection's epilogue on it, as the tiled kernel
+// does with its own sums.
+template <class Epi>
+__global__ void __launch_bounds__(256) split_epilogue_kernel(const float* P, int ks, int rows, int ldn, int n_tiles,
+                                                             int m_tiles, const float* bias, Epi epi) {
+    constexpr int RT = 16, WM = 4, LDY = 16 * WM + 1;
+    __shared__ float Y[16 * RT * LDY];
+    constexpr int ESM = Epi::kSmem > 0 ? Epi::kSmem : 16;
+    __shared__ __align__(16) char esm[ESM];
+    const int nt0 = blockIdx.x * RT, mt0 = blockIdx.y * WM;
+    const int nrows = 16 * min(RT, n_tiles - nt0), mcols = 16 * min(WM, m_tiles - mt0);
+    const int n0 = nt0 * 16, m0 = mt0 * 16;
+    const size_t slice = (size_t)rows * ldn;
+    // four consecutive outputs of one token per thread (16-byte loads along P's rows)
+    const int nq = nrows >> 2;
+    for (int idx = threadIdx.x; idx < nq * mcols; idx += blockDim.x) {
+        const int qd = idx % nq, ml = idx / nq, nl = 4 * qd;
+        const float* p = P + (size_t)(m0 + ml) * ldn + n0 + nl;
+        float4 v = *(const float4*)p;
+        for (int k = 1; k < ks; ++k) {
+            const float4 u = *(const float4*)(p + k * slice);
+            v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+        }
+        if (bias != nullptr) {
+            v.x += bias[n0 + nl]; v.y += bias[n0 + nl + 1]; v.z += bias[n0 + nl + 2]; v.w += bias[n0 + nl + 3];
+        }
+        Y[nl * LDY + ml] = v.x;
+        Y[(nl + 1) * LDY + ml] = v.y;
+        Y[(nl + 2) * LDY + ml] = v.z;
+        Y[(nl + 3) * LDY + ml] = v.w;
+    }
+    typename Epi::Pre pre;
+    epi.fetch(pre, n0, nrows, m0, mcols);
+    epi.stage(pre, esm, n0, nrows, m0, mcols);
+    __syncthreads();
+    epi(Y, LDY, n0, nrows, m0, mcols, blockIdx.x, esm, NoScale{});
+}
+
 }  // namespace dllm
