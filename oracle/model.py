@@ -295,20 +295,33 @@ class OracleModel:
 
 class OracleKV:
     """Per-layer K and V (after RoPE for K) of every cached position, float64,
-    [layer, position, K/V head, dim]."""
+    [layer, position, K/V head, dim].
 
-    def __init__(self, shape, capacity: int):
+    fp16=True stores every K/V value rounded to IEEE half precision (round to
+    nearest even), the paper's FP16 KV states (Implementation); the default keeps
+    them exact.  (Values past the half range would become infinite here; the tests
+    keep K and V far inside it.)"""
+
+    def __init__(self, shape, capacity: int, fp16: bool = False):
         L, H, dh = shape.n_layers, shape.kv_heads, shape.head_dim
         self.shape = shape
         self.capacity = capacity
+        self.fp16 = fp16
         self.K = np.zeros((L, capacity, H, dh))
         self.V = np.zeros((L, capacity, H, dh))
         self.prefix_len = 0
         self.prompt_len = 0
 
+    def store(self, layer: int, pos: np.ndarray, k: np.ndarray, v: np.ndarray) -> None:
+        if self.fp16:
+            k = k.astype(np.float16).astype(np.float64)
+            v = v.astype(np.float16).astype(np.float64)
+        self.K[layer, pos] = k
+        self.V[layer, pos] = v
+
     def copy(self) -> "OracleKV":
         c = OracleKV.__new__(OracleKV)
-        c.shape, c.capacity = self.shape, self.capacity
+        c.shape, c.capacity, c.fp16 = self.shape, self.capacity, self.fp16
         c.K, c.V = self.K.copy(), self.V.copy()
         c.prefix_len, c.prompt_len = self.prefix_len, self.prompt_len
         return c
@@ -352,8 +365,7 @@ def forward_rows(model: OracleModel, kv: OracleKV, ids: np.ndarray, pos: np.ndar
         v = (h @ w["wv"].T + w["bv"]).reshape(n, Hkv, dh)
         q = rope(q, pos, sh.rope_base)
         k = rope(k, pos, sh.rope_base)
-        kv.K[l, pos] = k
-        kv.V[l, pos] = v
+        kv.store(l, pos, k, v)
         o = attend(q, kv.K[l], kv.V[l], limits)
         x = x + o.reshape(n, H * dh) @ w["wo"].T
         h2 = rmsnorm(x, w["ffn_norm"], sh.eps)

@@ -259,6 +259,28 @@ def test_cached_prefix_equals_block_causal_recompute(sh):
     np.testing.assert_allclose(kv.V[:, :len(seq)], V, rtol=1e-10, atol=1e-12)
 
 
+def test_fp16_cache_stores_the_half_precision_rounding():
+    """OracleKV(fp16=True) rounds at storage and nowhere else: layer 0's K/V depend
+    only on the embeddings, so they are exactly numpy's round-to-nearest-even half
+    values of the exact run's; every stored value is a half-precision number; later
+    layers, which attend over the rounded cache, move by a small relative amount."""
+    sh = MICRO
+    model, _ = micro_model(sh)
+    prompt = synth.prompt_ids(sh, 20)
+    exact = oracle.OracleKV(sh, 20)
+    half = oracle.OracleKV(sh, 20, fp16=True)
+    oracle.prefill(model, exact, prompt)
+    oracle.prefill(model, half, prompt)
+    to_half = lambda a: a.astype(np.float16).astype(np.float64)
+    np.testing.assert_array_equal(half.K[0], to_half(exact.K[0]))
+    np.testing.assert_array_equal(half.V[0], to_half(exact.V[0]))
+    np.testing.assert_array_equal(half.K, to_half(half.K))
+    np.testing.assert_array_equal(half.V, to_half(half.V))
+    d = np.abs(half.K[1] - exact.K[1]).max()
+    assert 0 < d < 1e-2 * np.abs(exact.K[1]).max()
+    assert half.copy().fp16
+
+
 def test_block_mask_really_hides_the_future():
     """Changing a later block must not change earlier cached rows."""
     sh = MICRO
