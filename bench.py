@@ -4,8 +4,9 @@ Workload (default): one LLaDA-8B-shaped denoising step in bf16 with random
 N(0, 0.02) weights: 32 layers, d 4096, 32 heads x 128, SwiGLU 12288, vocab
 126464; a prefix KV cache of 512 tokens prefilled from random prompt ids; a
 32-token block with 24 MASK and 8 committed random ids; each step is
-dllm_denoise_step + dllm_commit(k=1).  Inputs are synthetic and resident in HBM
-before the timed region.
+dllm_denoise_step + dllm_commit(k=1), captured once as a HIP graph and replayed
+for the timed steps (--eager: plain library calls).  Inputs are synthetic and
+resident in HBM before the timed region.
 
 Prints ONE JSON line with the metric, a roofline record for the dominant kernel
 (gate/up projection: the largest share of a step's time) and the CPU oracle's
@@ -614,6 +615,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="default workload: skip the end-to-end, tiny-model, M-sweep and read-floor measurements "
                          "(short runs under a counter profiler)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time plain library calls instead of replays of the step captured as a HIP graph")
     ap.add_argument("--no-sls", action="store_true",
                     help="run the LM head over every window row (no selective logits skipping)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -695,8 +698,16 @@ def main():
         for j, (b, n, k) in enumerate(wl["segs"]):
             dl.dllm_commit(conf, ids, d_tok, d_mask, b, n, k, cpos[16 * j:], ncom[j:])
 
+    # The timed steps replay the step (its launches and the commits) captured once as a
+    # HIP graph: the same kernels with the same arguments, without the host's
+    # per-launch work (--eager: plain calls).
+    run = step
+    if not args.eager:
+        from paper_2606_13740_amd.graph import StepGraph
+
+        run = StepGraph(step).replay
     for _ in range(args.warmup):
-        step()
+        run()
     torch.cuda.synchronize()
     d_tok.copy_(d_tok0)
     d_mask.copy_(d_mask0)
@@ -705,7 +716,7 @@ def main():
     wall0 = time.perf_counter()
     e0.record()
     for _ in range(args.steps):
-        step()
+        run()
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -785,6 +796,7 @@ def main():
                    "d_ff": shape.d_ff, "vocab": shape.vocab,
                    "prefix": P, "window": W, "masked": len(wl["masked"]), "commits_per_step": commits,
                    "lm_head_rows": n_need if sls else W},
+        "launch": "eager library calls" if args.eager else "HIP graph replay of the step + commits",
         "query_tok_s": round(W * steps_s, 1),
         "committed_tok_s": round(commits * steps_s, 1),
         "step_hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
