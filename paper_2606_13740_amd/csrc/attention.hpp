@@ -169,11 +169,12 @@ attn_f16_kernel(AttnArgs a) {
     const int lim = (a.lim != nullptr && row < a.M) ? a.lim[row] : a.T;
 
     // Ring of NB buffers per key group: the group's first NB - 1 blocks are staged
-    // here (after the Q loads, so the ring's waits below see only block loads after
-    // them), and round t stages its block t + NB - 1 into the buffer round t - 1 used.
-    // With one key group every split has a block, and a split shorter than NB - 1
-    // blocks stages its last one again into the spare buffers: unconditional loads
-    // keep the compiler's own wait for the limit loads below from covering the blocks.
+    // here (after the Q loads, so the ring's waits below count only block loads issued
+    // after the block they wait for), and round t stages its block t + NB - 1 into the
+    // buffer round t - 1 used.  With one key group every split has a block, so its
+    // first block is staged without a test (a split shorter than NB - 1 blocks stages
+    // its last block again into the spare buffers, which nothing reads).  The compiler
+    // still waits for every load before the key-limit reads below.
     const int nmine = kb0 + grp < kb1 ? (kb1 - kb0 - grp + KS - 1) / KS : 0;
 #pragma unroll
     for (int j = 0; j < NB - 1; ++j) {
