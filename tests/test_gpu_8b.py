@@ -86,8 +86,10 @@ def _run(shape, dtype, P, W, masked, cap_extra=0, sls=False):
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("dtype,P,W", [("bf16", 512, 32), ("bf16", 512, 48), ("bf16", 1024, 64), ("w8", 512, 64),
-                                       ("q4", 512, 32), ("q4", 512, 48), ("q4", 512, 64)])
+                                       ("q4", 512, 32), ("q4", 512, 48), ("q4", 512, 64), ("bf16", 440, 32)])
 def test_8b_width_two_layers(dtype, P, W):
+    """The bench's launches at the 8B widths; the 440-token prompt (448 rows) takes the
+    prompt's split-K QKV with a ragged second token group (12 of 16 token tiles)."""
     masked = list(range(8, 32)) if W == 32 else list(range(24, W))
     _run(BIG.with_layers(2), dtype, P, W, masked)
 
