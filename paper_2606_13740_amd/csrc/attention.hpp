@@ -376,10 +376,11 @@ attn_f16_kernel(AttnArgs a) {
 }
 
 // Merge key-range splits: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M).
-// 32 lanes per (row, head), four consecutive dims per lane; ATTN_MERGE_PAIRS (row,
-// head) pairs per workgroup: 4, so that a 32-row window over 32 heads gives every CU
-// one workgroup (LLaDA-8B, 32 rows: attention + merge 13.8 -> 12.1 us per layer
-// against 8 pairs and 128 workgroups; 2 pairs and 512 workgroups: no gain).
+// 32 lanes per (row, head), four consecutive dims per lane (head dims <= 128);
+// ATTN_MERGE_PAIRS (row, head) pairs per workgroup: 4, so that a 32-row window over
+// 32 heads gives every CU one workgroup (LLaDA-8B, 32 rows: attention + merge 13.8 ->
+// 12.1 us per layer against 8 pairs and 128 workgroups; 2 pairs and 512 workgroups:
+// no gain).
 constexpr int ATTN_MERGE_PAIRS = 4;
 template <bool XF32>
 __global__ void __launch_bounds__(32 * ATTN_MERGE_PAIRS) attn_combine_kernel(AttnArgs a, int rows, int DH) {
@@ -390,12 +391,19 @@ __global__ void __launch_bounds__(32 * ATTN_MERGE_PAIRS) attn_combine_kernel(Att
     const int h = pair % a.H, row = pair / a.H;
     const size_t stride_s = (size_t)a.rows_ld * a.H;          // (row, head) records per split
     const size_t rec = (size_t)row * a.H + h;
-    // issue every split's loads before using any of them
+    const int d0 = 4 * l;
+    const bool has_d = d0 < DH;
+    // every split's (m, l) and output loads go out before any is used: one memory
+    // round trip
     float2 ml[MAXS];
+    float4 v[MAXS];
 #pragma unroll
-    for (int s = 0; s < MAXS; ++s)
+    for (int s = 0; s < MAXS; ++s) {
         ml[s] = (s < a.nsplit) ? *(const float2*)(a.mlpart + (s * stride_s + rec) * 2)
                                : make_float2(-INFINITY, 0.f);
+        v[s] = (s < a.nsplit && has_d) ? *(const float4*)(a.opart + (s * stride_s + rec) * DH + d0)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int s = 0; s < MAXS; ++s) mx = fmaxf(mx, ml[s].x);
@@ -406,19 +414,13 @@ __global__ void __launch_bounds__(32 * ATTN_MERGE_PAIRS) attn_combine_kernel(Att
         L += ml[s].y * w[s];
     }
     const float inv = 1.f / L;
-    for (int d0 = 4 * l; d0 < DH; d0 += 128) {
-        float4 v[MAXS];
+    if (!has_d) return;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int s = 0; s < MAXS; ++s)
-            v[s] = (s < a.nsplit) ? *(const float4*)(a.opart + (s * stride_s + rec) * DH + d0)
-                                  : make_float4(0.f, 0.f, 0.f, 0.f);
-        float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int s = 0; s < MAXS; ++s) {
-            o.x += v[s].x * w[s]; o.y += v[s].y * w[s]; o.z += v[s].z * w[s]; o.w += v[s].w * w[s];
-        }
-        xfrag_store4<XF32>(a.o, row, h * DH + d0, a.KCx, make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv));
+    for (int s = 0; s < MAXS; ++s) {
+        o.x += v[s].x * w[s]; o.y += v[s].y * w[s]; o.z += v[s].z * w[s]; o.w += v[s].w * w[s];
     }
+    xfrag_store4<XF32>(a.o, row, h * DH + d0, a.KCx, make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv));
 }
 
 // fp32 path (small models): one wave per (row, head); lanes stride over keys with

@@ -577,8 +577,17 @@ int residual_proj(dllm_model* m, Workspace& w, const PackedW& W, const void* X, 
     EpiPartial e{w.part, d, Mc};
     int rc = launch_gemm<WT, G_RES>(dc, W.n_tiles, MT, g, e, gy, s);
     if (rc) return rc;
-    hipLaunchKernelGGL((residual_reduce_kernel<XF32>), dim3(Mc), dim3(ROW_NT), 0, s, (const float*)w.part, KS, Mc, d,
-                       M, m->cfg.eps, w.x, gnext, w.xg, m->KCx_d, sel, need, n_sel);
+#define RRED(KS_)                                                                                              \
+    hipLaunchKernelGGL((residual_reduce_kernel<XF32, KS_>), dim3(Mc), dim3(ROW_NT), 0, s, (const float*)w.part, Mc, \
+                       d, M, m->cfg.eps, w.x, gnext, w.xg, m->KCx_d, sel, need, n_sel)
+    switch (KS) {
+        case 1: RRED(1); break;
+        case 2: RRED(2); break;
+        case 4: RRED(4); break;
+        case 8: RRED(8); break;
+        default: return fail(DLLM_E_INVAL, "internal: K slices of a residual projection not 1, 2, 4 or 8");
+    }
+#undef RRED
     return DLLM_OK;
 }
 

@@ -25,10 +25,12 @@ __device__ __forceinline__ float block_sum(float v, float* red /* NT/64 */) {
 }
 
 // With ssq != nullptr (RMSNorm folded into the consumer GEMM) the operand is x * g,
-// not normalised, and the row's sum of x^2 goes to *ssq for the consumer.
+// not normalised, and the row's sum of x^2 goes to *ssq for the consumer.  The
+// caller loads the gain gv with the row (one memory round trip, not a second one
+// after the block sum's barriers).
 template <bool XF32, int NT, int VPT>
-__device__ __forceinline__ void write_norm_operand(const float4 (&xv)[VPT], int m, int d, float eps, const float* g,
-                                                   void* xg, int KCx, float* red, float* ssq = nullptr) {
+__device__ __forceinline__ void write_norm_operand(const float4 (&xv)[VPT], const float4 (&gv)[VPT], int m, int d,
+                                                   float eps, void* xg, int KCx, float* red, float* ssq = nullptr) {
     float sq = 0.f;
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
@@ -42,7 +44,7 @@ __device__ __forceinline__ void write_norm_operand(const float4 (&xv)[VPT], int 
     for (int j = 0; j < VPT; ++j) {
         const int n = 4 * (threadIdx.x + j * NT);
         if (n >= d) continue;
-        const float4 gg = *(const float4*)(g + n);
+        const float4 gg = gv[j];
         xfrag_store4<XF32>(xg, m, n, KCx,
                            make_float4(xv[j].x * rs * gg.x, xv[j].y * rs * gg.y, xv[j].z * rs * gg.z,
                                        xv[j].w * rs * gg.w));
@@ -82,7 +84,7 @@ embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int
         const int sl = lm_slot<ROW_NT>(need, n_sel, M, m, red);
         if (threadIdx.x == 0) slot[m] = sl;
     }
-    float4 xv[ROW_VPT];
+    float4 xv[ROW_VPT], gv[ROW_VPT];
     int id = -1;
     if (m < M) {
         id = (mask != nullptr && mask[m]) ? mask_id : tok[m];
@@ -91,15 +93,19 @@ embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int
 #pragma unroll
     for (int j = 0; j < ROW_VPT; ++j) {
         const int n = 4 * (threadIdx.x + j * ROW_NT);
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (n < d && id >= 0) {
-            const ET* row = E + (size_t)id * d + n;
-            v = make_float4(to_f32<ET>(row[0]), to_f32<ET>(row[1]), to_f32<ET>(row[2]), to_f32<ET>(row[3]));
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f), gg = v;
+        if (n < d) {
+            gg = *(const float4*)(g + n);
+            if (id >= 0) {
+                const ET* row = E + (size_t)id * d + n;
+                v = make_float4(to_f32<ET>(row[0]), to_f32<ET>(row[1]), to_f32<ET>(row[2]), to_f32<ET>(row[3]));
+            }
+            *(float4*)(x + (size_t)m * d + n) = v;
         }
         xv[j] = v;
-        if (n < d) *(float4*)(x + (size_t)m * d + n) = v;
+        gv[j] = gg;
     }
-    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, m, d, eps, g, xg, KCx, red,
+    write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, gv, m, d, eps, xg, KCx, red,
                                               ssq != nullptr ? ssq + (size_t)m * ssq_ld : nullptr);
 }
 
@@ -107,39 +113,39 @@ embed_kernel(const ET* E, const int* tok, const uint8_t* mask, int M, int d, int
 //   x[m][n] += sum_ks P[ks][m][n]   (fixed order),
 // then the next RMSNorm's normalised operand.  Padding rows get zeros.  With
 // `sel` set (the last layer feeding a selective LM head) the operand of a kept row
-// goes to its slot (lm_slot) and other rows write none.
-template <bool XF32>
+// goes to its slot (lm_slot) and other rows write none.  KS (the K slices) is a
+// template argument so that the slices, the residual and the gain are loaded
+// without a condition each, in one round (a select per slice made the compiler
+// wait for the first loads before issuing the rest).
+template <bool XF32, int KS>
 __global__ void __launch_bounds__(ROW_NT)
-residual_reduce_kernel(const float* P, int KS, int prow, int d, int M, float eps, float* x, const float* g,
+residual_reduce_kernel(const float* P, int prow, int d, int M, float eps, float* x, const float* g,
                        void* xg, int KCx, bool sel, const uint8_t* need, int n_sel) {
     __shared__ float red[ROW_NT / 64];
     const int m = blockIdx.x;
-    int dst = m;
-    if (sel) {
-        dst = lm_slot<ROW_NT>(need, n_sel, M, m, red);
-    }
-    float4 xv[ROW_VPT];
+    float4 xv[ROW_VPT], gv[ROW_VPT];
 #pragma unroll
     for (int j = 0; j < ROW_VPT; ++j) {
         const int n = 4 * (threadIdx.x + j * ROW_NT);
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f), gg = v;
         if (n < d && m < M) {
             float4* xp = (float4*)(x + (size_t)m * d + n);
-            float4 p[8];
+            float4 p[KS];
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks)
-                p[ks] = (ks < KS) ? *(const float4*)(P + ((size_t)ks * prow + m) * d + n)
-                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int ks = 0; ks < KS; ++ks) p[ks] = *(const float4*)(P + ((size_t)ks * prow + m) * d + n);
             v = *xp;
+            gg = *(const float4*)(g + n);
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
+            for (int ks = 0; ks < KS; ++ks) {
                 v.x += p[ks].x; v.y += p[ks].y; v.z += p[ks].z; v.w += p[ks].w;
             }
             *xp = v;
         }
         xv[j] = v;
+        gv[j] = gg;
     }
-    if (dst >= 0) write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, dst, d, eps, g, xg, KCx, red);
+    const int dst = sel ? lm_slot<ROW_NT>(need, n_sel, M, m, red) : m;
+    if (dst >= 0) write_norm_operand<XF32, ROW_NT, ROW_VPT>(xv, gv, dst, d, eps, xg, KCx, red);
 }
 
 // Zeroes the padding columns [kreal, KCx * columns per chunk) of an activation
