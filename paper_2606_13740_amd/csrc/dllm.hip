@@ -709,8 +709,8 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 // prefix 1024: 17.5 against 20.0 us per layer for one key group.  For 32
                 // rows, and for long prefixes, one group per workgroup and the most splits
                 // are faster (prefix 512: 13.3 against 14.9-15.8 us; 4096: 32.4 against 34.1).
-                const int QGs = Mc / 16;
-                const int KSs = QGs <= 2 ? 4 : 2;
+                const int QGs = Mc / 16;                   // 3 or 4
+                const int KSs = 2;
                 const int nblk = ceil_div(a.T, 32);
                 int nsplit = std::min(ceil_div(nblk, KSs * ATTN_ROUNDS), MAX_SPLIT);
                 at.bps = ceil_div(nblk, nsplit);
@@ -718,8 +718,7 @@ int forward_t(dllm_model* m, dllm_kv* kv, const FwdArgs& a, hipStream_t s) {
                 dim3 grid(at.nsplit * H);
 #define ATTN_W(DH_, QG_, KS_) hipLaunchKernelGGL((attn_f16_kernel<DH_, QG_, KS_, 2>), grid, dim3(QG_ * KS_ * 64), 0, s, at)
 #define ATTN_W_QG(DH_) \
-    do { if (QGs == 1) ATTN_W(DH_, 1, 4); else if (QGs == 2) ATTN_W(DH_, 2, 4); \
-         else if (QGs == 3) ATTN_W(DH_, 3, 2); else ATTN_W(DH_, 4, 2); } while (0)
+    do { if (QGs == 3) ATTN_W(DH_, 3, 2); else ATTN_W(DH_, 4, 2); } while (0)
                 if (Dh == 128) ATTN_W_QG(128); else ATTN_W_QG(64);
 #undef ATTN_W_QG
 #undef ATTN_W
