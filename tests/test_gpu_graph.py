@@ -1,5 +1,7 @@
 """Steps replayed from a captured HIP graph (paper_2606_13740_amd.graph.StepGraph)
-against the same steps run eagerly.
+against the same steps run eagerly: the 32-row step + commit, and the 64-row speculative
+window step with selective logits + per-segment commits (bf16 and int8 weights, and the
+int8 workload's 8B-width launch at prefix 4096 with its 15-split attention).
 
 A replay launches exactly the captured kernels, so every replay must be
 bit-identical to the eager call from the same state.  Each test replays several
@@ -114,3 +116,64 @@ def test_step_graph_at_8b_width_equals_eager():
         _other_eager_work(model, kv, tok, mask)
     kv.close()
     model.close()
+
+
+def _spec_step_graph(shape, dtype, P, W, masked, segs, n):
+    """The speculative window step as the 64-row workloads run it: dllm_denoise_window_sls over
+    the masked rows (LM head over at most n_need of them) and one dllm_commit per segment,
+    replayed n times against the same sequence run eagerly from the same state."""
+    model, kv, tok, mask = _setup(shape, dtype, P, W, masked)
+    d_tok0, d_mask0 = dev_i32(tok), dev_u8(mask)
+    d_tok, d_mask = d_tok0.clone(), d_mask0.clone()
+    n_need = len(masked)
+    ids = torch.empty(W, dtype=torch.int32, device="cuda")
+    conf = torch.empty(W, device="cuda")
+    cpos = torch.empty(16 * len(segs), dtype=torch.int32, device="cuda")
+    ncom = torch.empty(len(segs), dtype=torch.int32, device="cuda")
+
+    def step():
+        dl.dllm_denoise_window_sls(model.handle, kv.handle, P, d_tok, d_mask, d_mask, n_need, W, ids, conf)
+        for j, (b, ln, k) in enumerate(segs):
+            dl.dllm_commit(conf, ids, d_tok, d_mask, b, ln, k, cpos[16 * j:], ncom[j:])
+
+    def reset():
+        d_tok.copy_(d_tok0)
+        d_mask.copy_(d_mask0)
+        torch.cuda.synchronize()
+
+    def snapshot():
+        return [t.cpu().numpy().copy() for t in (ids, conf, d_tok, d_mask, ncom)]
+
+    eager = []
+    for _ in range(n):
+        step()
+        torch.cuda.synchronize()
+        eager.append(snapshot())
+    reset()
+    g = StepGraph(step)
+    reset()
+    for i in range(n):
+        ids.fill_(-7)
+        conf.fill_(-1.0)
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(snapshot(), eager[i]):
+            np.testing.assert_array_equal(a, b)
+        _other_eager_work(model, kv, tok, mask)
+    committed = sum(k for _, _, k in segs) * n
+    assert int(d_mask.sum()) == len(masked) - committed           # the commits really happened
+    kv.close()
+    model.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "w8"])
+def test_spec_window_step_replays_equal_eager_steps(dtype):
+    print(f"case: graph of the 64-row SLS step + 2 segment commits, {dtype}, prefix 160", flush=True)
+    _spec_step_graph(synth.SMALL_BF16, dtype, 160, 64, list(range(8, 64)), [(0, 32, 2), (32, 32, 2)], 6)
+
+
+def test_spec_window_step_graph_at_8b_width_int8_prefix_4096():
+    """The int8 64-row workload's launch configuration (8B widths, prefix 4096: the 15-split
+    attention and its merge; 2 layers)."""
+    print("case: graph of the int8 64-row SLS step at 8B width, prefix 4096", flush=True)
+    _spec_step_graph(synth.LLADA_8B.with_layers(2), "w8", 4096, 64, list(range(0, 64)), [(0, 32, 2), (32, 32, 2)], 3)
