@@ -112,6 +112,14 @@ def test_8b_full_depth_step():
 
 @pytest.mark.slow
 @pytest.mark.timeout(900)
+def test_8b_full_depth_q4_step():
+    """32 layers of Q4_0 weights (the converter's codes and fp16 block scales), the
+    32-row window at prefix 512 that the Q4_0 workload times."""
+    _run(BIG, "q4", 512, 32, list(range(8, 32)))
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
 def test_8b_full_depth_int8_spec_window_sls():
     """32 layers of int8 weights, a 64-row all-MASK window (current + speculative
     block) through the benchmark's selective-logits call, prefix 512."""
