@@ -132,13 +132,11 @@ def test_gqa_refresh_matches_oracle(pair):
     kv.close()
 
 
-@pytest.mark.timeout(600)
-@pytest.mark.parametrize("dtype,W", [("bf16", 32), ("bf16", 64)])
-def test_dream7b_width_two_layers(dtype, W):
-    sh = synth.DREAM_7B.with_layers(2)
+def _dream_run(n_layers, dtype, W):
+    sh = synth.DREAM_7B.with_layers(n_layers)
     P = 512
-    print(f"case: Dream-7B width {dtype}, 2 layers, prefix {P}, window {W}", flush=True)
-    layers = [synth.layer_weights(sh, l, "bf16") for l in range(2)]
+    print(f"case: Dream-7B width {dtype}, {n_layers} layers, prefix {P}, window {W}", flush=True)
+    layers = [synth.layer_weights(sh, l, "bf16") for l in range(n_layers)]
     glob = synth.global_weights(sh, "bf16")
     model = dl.Model(sh, dtype, glob, lambda l: layers[l], max_window=64, max_pos=P + W + 64)
     kv = dl.KVCache(model, P + W)
@@ -158,3 +156,17 @@ def test_dream7b_width_two_layers(dtype, W):
     np.testing.assert_allclose(conf, ref.conf, rtol=0.2)
     kv.close()
     model.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("dtype,W", [("bf16", 32), ("bf16", 64)])
+def test_dream7b_width_two_layers(dtype, W):
+    _dream_run(2, dtype, W)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_dream7b_full_depth_step():
+    """All 28 layers of the Dream-7B shape (grouped-query attention over 4 K/V heads, Q/K/V
+    biases), the 32-row window at prefix 512 that its workload times."""
+    _dream_run(synth.DREAM_7B.n_layers, "bf16", 32)
