@@ -231,16 +231,19 @@ lm_combine_kernel(const LmPartial* part, int n_wg, int part_ld, int* out_id, flo
         }
         m = slot;
     }
+    // Lane l merges records l, l + 64, l + 128, ... in that order.  The loads of a round
+    // go out together, unconditionally (an index past the last record reloads the last
+    // one, which the merge then skips): with a select per load the compiler waited for
+    // the first loads before issuing the rest.
     LmPartial acc{-INFINITY, -1, 0.f, 0.f};
-    for (int w0 = lane; w0 < n_wg; w0 += 64 * 8) {
-        LmPartial q[8];
+    constexpr int R = 16;
+    for (int w0 = lane; w0 < n_wg; w0 += 64 * R) {
+        LmPartial q[R];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int w = w0 + 64 * j;
-            q[j] = (w < n_wg) ? part[(size_t)w * part_ld + m] : LmPartial{-INFINITY, -1, 0.f, 0.f};
-        }
+        for (int j = 0; j < R; ++j) q[j] = part[(size_t)min(w0 + 64 * j, n_wg - 1) * part_ld + m];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc = lm_merge(acc, q[j]);
+        for (int j = 0; j < R; ++j)
+            if (w0 + 64 * j < n_wg) acc = lm_merge(acc, q[j]);
     }
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
