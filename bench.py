@@ -35,7 +35,7 @@ WORKLOADS = {
                                         masked=list(range(24, 64)), segs=[(0, 32, 4), (32, 32, 4)], sls=True),
     "llada8b_w8_p4096_w64_spec": dict(shape="llada8b", dtype="w8", prefix=4096, W=64,
                                       masked=list(range(0, 64)), segs=[(0, 32, 2), (32, 32, 2)], sls=True),
-    # Q4_0 weights (the paper's own quantisation), otherwise config 2
+    # Q4_0 weights (the paper's own quantisation), otherwise the bf16 step at prefix 512, 32 rows
     "llada8b_q4_p512_w32": dict(shape="llada8b", dtype="q4", prefix=512, W=32,
                                 masked=list(range(8, 32)), segs=[(0, 32, 1)]),
     # Dream-7B (grouped-query attention, 28 query heads over 4 K/V heads, Q/K/V biases)

@@ -137,7 +137,7 @@ constexpr int activation_depth() {
 // Reduction slots: the largest power of two <= NWk whose slots fit ~150 KiB of LDS (a
 // workgroup of these layouts has its CU to itself).  With one slot per wave the
 // K-slice sums take one write round: LLaDA-8B down at 32 rows (8 slots of 16.5 KiB)
-// 26.9 -> 26.2 us, config-2 step 3.99 -> 3.97 ms, against a 100 KiB budget.
+// 26.9 -> 26.2 us, 32-row step at prefix 512 3.99 -> 3.97 ms, against a 100 KiB budget.
 template <int NWk>
 constexpr int reduce_slots(int slot_bytes) {
     int s = NWk;
