@@ -141,3 +141,50 @@ def test_8b_full_depth_bf16_spec_window_prefix_1024():
     """32 layers, bf16, prefix 1024, a 64-row window with 8 MASK in the current block
     and an all-MASK speculative block, through the selective-logits call."""
     _run(BIG, "bf16", 1024, 64, list(range(24, 64)), sls=True)
+
+
+@pytest.mark.timeout(600)
+def test_8b_width_append_and_refresh():
+    """The end-to-end generation's cache calls at the 8B widths (2 layers): a 512-token
+    prefill, two 32-token block appends, then a sparse refresh of 4 revised positions (two
+    in the prompt, two in the appended blocks: 4 rows with their own key limits) with
+    its LM-head outputs.  The whole cache and the refresh's ids / confidences against the
+    oracle."""
+    sh = BIG.with_layers(2)
+    P0, B = 512, sh.block
+    cap = P0 + 2 * B
+    print(f"case: 8B-width bf16, 2 layers, prefill {P0}, 2 appends of {B}, refresh of 4 rows", flush=True)
+    layers = [synth.layer_weights(sh, l, "bf16") for l in range(sh.n_layers)]
+    glob = synth.global_weights(sh, "bf16")
+    model = dl.Model(sh, "bf16", glob, lambda l: layers[l], max_window=64, max_pos=cap + 64)
+    kv = dl.KVCache(model, cap)
+    om = oracle.OracleModel(sh, dict(glob, layers=layers), cache_layers=True)
+    okv = oracle.OracleKV(sh, cap)
+    prompt = synth.prompt_ids(sh, P0)
+    dl.dllm_prefill(model.handle, kv.handle, dev_i32(prompt), P0)
+    oracle.prefill(om, okv, prompt)
+    for b in range(2):
+        blk = synth.uniform_ids(90 + b, 1, B, sh.mask_id)
+        dl.dllm_append_prefix_kv(model.handle, kv.handle, dev_i32(blk), B)
+        oracle.append_block(om, okv, blk)
+    pos = np.array([P0 + 3, 7, P0 + B + 30, P0 + B], np.int32)
+    new = synth.uniform_ids(95, 1, 4, sh.mask_id)
+    ids = torch.empty(4, dtype=torch.int32, device="cuda")
+    conf = torch.empty(4, device="cuda")
+    dl.dllm_refresh_kv(model.handle, kv.handle, dev_i32(pos), dev_i32(new), 4, ids, conf)
+    torch.cuda.synchronize()
+    assert kv.prefix_len == cap
+    r_ids, r_conf, r_logits = oracle.refresh(om, okv, pos, new, lm_head=True)
+    K, Vt = kv.views()
+    Kg = K[:, :, :cap].float().cpu().numpy()                      # [L, Hkv, n, Dh]
+    Vg = Vt[:, :, :, :cap].float().cpu().numpy()                  # [L, Hkv, Dh, n]
+    Kr = np.transpose(okv.K[:, :cap], (0, 2, 1, 3))
+    Vr = np.transpose(okv.V[:, :cap], (0, 2, 3, 1))
+    err = max(float(np.abs(Kg - Kr).max()), float(np.abs(Vg - Vr).max()))
+    print(f"  cache max |dK|, |dV| = {err:.3e}", flush=True)
+    np.testing.assert_allclose(Kg, Kr, atol=5e-2, rtol=5e-2)
+    np.testing.assert_allclose(Vg, Vr, atol=5e-2, rtol=5e-2)
+    np.testing.assert_allclose(conf.cpu().numpy(), r_conf, rtol=0.1)
+    assert_ids_match_where_decided(ids.cpu().numpy(), r_logits, 5e-2)
+    kv.close()
+    model.close()
