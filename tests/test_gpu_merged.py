@@ -43,13 +43,18 @@ def _merged(model, kv, ref_pos, ref_new, blk, tok, mask):
             rout[0].cpu().numpy()[:n_ref], rout[1].cpu().numpy()[:n_ref].astype(np.float64))
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_merged_matches_sequential_oracle(dtype):
-    sh = synth.MICRO if dtype == "f32" else synth.SMALL_BF16
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("case", ["f32", "bf16", "bf16_8b_width"])
+def test_merged_matches_sequential_oracle(case):
+    """Small shapes, and the 8B widths (2 layers) near the merged generation's configuration:
+    a 512-token prompt, 4 refresh rows + a 32-token block + a 28-row window (64 rows, the
+    models' window limit)."""
+    dtype = "f32" if case == "f32" else "bf16"
+    sh = {"f32": synth.MICRO, "bf16": synth.SMALL_BF16, "bf16_8b_width": synth.LLADA_8B.with_layers(2)}[case]
     atol, crtol = (1e-4, 1e-3) if dtype == "f32" else (5e-2, 0.1)
-    model, om, _ = build_pair(sh, dtype, max_pos=512)
-    B, P0, W = sh.block, 40, 20
+    B, P0, W = (sh.block, 512, 28) if case == "bf16_8b_width" else (sh.block, 40, 20)
     cap = P0 + 3 * B + W
+    model, om, _ = build_pair(sh, dtype, max_pos=max(512, cap + 64))
     kv = dl.KVCache(model, cap)
     okv = oracle.OracleKV(sh, cap)
     prompt = synth.prompt_ids(sh, P0)
@@ -63,7 +68,7 @@ def test_merged_matches_sequential_oracle(dtype):
     ref_new = synth.uniform_ids(81, 1, 4, sh.mask_id)
     blk2 = synth.uniform_ids(71, 1, B, sh.mask_id)
     tok, mask = synth.window(sh, W, range(4, W))
-    print(f"case: merged {dtype}: 4 refresh + {B} append + {W} window rows at prefix {P}", flush=True)
+    print(f"case: merged {case}: 4 refresh + {B} append + {W} window rows at prefix {P}", flush=True)
     ids, conf, rids, rconf = _merged(model, kv, ref_pos, ref_new, blk2, tok, mask)
     r_ids, r_conf, r_logits = oracle.refresh(om, okv, ref_pos, ref_new, lm_head=True)
     oracle.append_block(om, okv, blk2)
